@@ -1,0 +1,447 @@
+/*
+ * bp_oracle.cpp -- CPU oracle for pooled back-propagation.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load or run this file.  It shares no code,
+ * header, table or helper with the HIP library, and the library never calls
+ * it.
+ *
+ * It is a plain, slow, obviously correct implementation of what the paper's
+ * simulator computes (Witbrock & Zagha, "An Implementation of
+ * Back-Propagation Learning on GF11", CMU-CS-89-208):
+ *
+ *   forward   a_{l+1}[j] = sigma( W_l[n_l][j] + sum_i a_l[i] * W_l[i][j] )
+ *             -- a unit's net input is the weighted sum of the activations
+ *             feeding it (section 3); the always-on "true unit" feeds every
+ *             non-input layer (section 6.3), stored as the last row of W_l;
+ *             sigma(x) = 1 / (1 + e^-x) (section 3, footnote 4).
+ *   error     e = t - y, reported error = sum over patterns and outputs of e^2
+ *             ("summed squared difference", section 3 footnote 5; "total
+ *             squared error", section 8).
+ *   deltas    delta_L = e * y * (1 - y); for l = L-1 .. 1:
+ *             delta_l[i] = a_l[i] (1 - a_l[i]) * sum_j W_l[i][j] delta_{l+1}[j]
+ *             -- partial derivatives taken from the output weights backwards
+ *             (section 3); input units get no back-propagated error (the
+ *             backward cycle count of section 6.1 charges input connections
+ *             one add and one multiply only); the bias row is not used.
+ *   pooled    G_l[i][j] = sum over the patterns of a batch of
+ *             a_l[i] * delta_{l+1}[j]  (bias row: sum of delta_{l+1}[j]),
+ *             i.e. the weight changes of all patterns summed and applied once
+ *             (sections 3 and 4.1).
+ *   update    V_l = lr * G_l + momentum * V_l ;  W_l += V_l
+ *             -- learning rate and momentum applied to the summed change,
+ *             with the previous change kept (sections 6.2.1 and 9).
+ *
+ * Readings where the paper is silent (each is listed with its reason in the
+ * design notes): the batch change is the SUM (not the mean) over patterns;
+ * delta carries no factor 2 (the gradient is that of half the squared error,
+ * while the reported error has no half); momentum in the classical form above;
+ * V starts at zero and persists across batches and epochs; a short last batch
+ * is applied like any other; patterns are taken in order; the exact logistic.
+ *
+ * Precision: the net is templated on the STORAGE type Real (float or double).
+ * Weights, momentum, activations and deltas are stored as Real; every sum
+ * (net input, delta dot product, batch sum, error) uses a double accumulator,
+ * sigma is evaluated in double and then rounded to Real.  The double instance
+ * is the plain definition; the float instance rounds at the storage points a
+ * float32 implementation has, which measures the float32 noise floor.
+ *
+ * Parallelism (OpenMP) only splits independent work: patterns in the forward
+ * and backward passes, and output rows in the batch sum, where every element
+ * is still accumulated over the patterns in pattern order.  Results do not
+ * depend on the thread count.
+ */
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <type_traits>
+#include <vector>
+
+#include <omp.h>
+
+namespace {
+
+template <typename Real>
+struct Net {
+  int L = 0;                    // number of weight layers
+  std::vector<int> n;           // n[0..L]
+  std::vector<int64_t> off;     // offset of W_l in the flat arrays
+  int64_t total = 0;            // sum (n_l + 1) * n_{l+1}
+  std::vector<Real> W, V;       // flat, layer l row-major (n_l + 1) x n_{l+1}
+
+  const Real* w(int l) const { return W.data() + off[l]; }
+  Real* w(int l) { return W.data() + off[l]; }
+  Real* v(int l) { return V.data() + off[l]; }
+};
+
+double sigmoid(double z) { return 1.0 / (1.0 + std::exp(-z)); }
+
+// Per-batch state: activations a_0..a_L and deltas delta_1..delta_L of every
+// pattern, stored row by row ([pattern][unit]).
+template <typename Real>
+struct BatchState {
+  std::vector<std::vector<Real>> a;    // a[l] : rows x n_l
+  std::vector<std::vector<Real>> d;    // d[l] : rows x n_l (l >= 1)
+  std::vector<double> sse_p;           // squared error of each pattern
+};
+
+// Forward pass of one pattern: a[0] already holds the inputs.
+template <typename Real>
+void forward_pattern(const Net<Real>& net, std::vector<Real*>& a) {
+  for (int l = 0; l < net.L; ++l) {
+    const int n_in = net.n[l], n_out = net.n[l + 1];
+    const Real* W = net.w(l);
+    std::vector<double> acc(n_out);
+    for (int j = 0; j < n_out; ++j) acc[j] = (double)W[(int64_t)n_in * n_out + j];  // true unit
+    for (int i = 0; i < n_in; ++i) {
+      const double ai = (double)a[l][i];
+      const Real* row = W + (int64_t)i * n_out;
+      for (int j = 0; j < n_out; ++j) acc[j] += ai * (double)row[j];
+    }
+    for (int j = 0; j < n_out; ++j) a[l + 1][j] = (Real)sigmoid(acc[j]);
+  }
+}
+
+// Deltas of one pattern from its activations and target; returns sum e^2.
+template <typename Real>
+double backward_pattern(const Net<Real>& net, Real* const* a, Real* const* d, const float* t) {
+  const int L = net.L, nL = net.n[L];
+  double sse = 0.0;
+  for (int k = 0; k < nL; ++k) {
+    const double y = (double)a[L][k];
+    const double e = (double)t[k] - y;
+    sse += e * e;
+    d[L][k] = (Real)(e * y * (1.0 - y));
+  }
+  for (int l = L - 1; l >= 1; --l) {
+    const int n_in = net.n[l], n_out = net.n[l + 1];
+    const Real* W = net.w(l);
+    for (int i = 0; i < n_in; ++i) {
+      const Real* row = W + (int64_t)i * n_out;
+      double s = 0.0;
+      for (int j = 0; j < n_out; ++j) s += (double)row[j] * (double)d[l + 1][j];
+      const double ai = (double)a[l][i];
+      d[l][i] = (Real)(ai * (1.0 - ai) * s);
+    }
+  }
+  return sse;
+}
+
+// Forward and backward passes for `rows` patterns whose inputs are already in
+// st.a[0].  With t == nullptr only the forward pass runs.
+template <typename Real>
+void run_batch(const Net<Real>& net, BatchState<Real>& st, int64_t rows, const float* t) {
+  const int L = net.L;
+#pragma omp parallel for schedule(static)
+  for (int64_t p = 0; p < rows; ++p) {
+    std::vector<Real*> a(L + 1), d(L + 1, nullptr);
+    for (int l = 0; l <= L; ++l) a[l] = st.a[l].data() + p * net.n[l];
+    forward_pattern(net, a);
+    if (t) {
+      for (int l = 1; l <= L; ++l) d[l] = st.d[l].data() + p * net.n[l];
+      st.sse_p[p] = backward_pattern(net, a.data(), d.data(), t + p * net.n[L]);
+    }
+  }
+}
+
+// G_l[i][j] = sum_p a_l[p][i] * delta_{l+1}[p][j]; row n_l (true unit) = sum_p delta.
+// Rows are split among threads; each element sums the patterns in order.
+template <typename Real>
+void batch_sum(const Net<Real>& net, const BatchState<Real>& st, int64_t rows, double* G) {
+  for (int l = 0; l < net.L; ++l) {
+    const int n_in = net.n[l], n_out = net.n[l + 1];
+    double* Gl = G + net.off[l];
+    const Real* A = st.a[l].data();
+    const Real* D = st.d[l + 1].data();
+#pragma omp parallel
+    {
+      const int nt = omp_get_num_threads(), tid = omp_get_thread_num();
+      const int r0 = (int)((int64_t)(n_in + 1) * tid / nt);
+      const int r1 = (int)((int64_t)(n_in + 1) * (tid + 1) / nt);
+      for (int i = r0; i < r1; ++i)
+        for (int j = 0; j < n_out; ++j) Gl[(int64_t)i * n_out + j] = 0.0;
+      for (int64_t p = 0; p < rows; ++p) {
+        const Real* dp = D + p * n_out;
+        for (int i = r0; i < r1; ++i) {
+          const double ai = (i < n_in) ? (double)A[p * n_in + i] : 1.0;
+          double* g = Gl + (int64_t)i * n_out;
+          for (int j = 0; j < n_out; ++j) g[j] += ai * (double)dp[j];
+        }
+      }
+    }
+  }
+}
+
+template <typename Real>
+void apply_update(Net<Real>& net, const double* G, double lr, double mom) {
+  const int64_t total = net.total;
+  Real* W = net.W.data();
+  Real* V = net.V.data();
+#pragma omp parallel for schedule(static)
+  for (int64_t k = 0; k < total; ++k) {
+    const Real v = (Real)(lr * G[k] + mom * (double)V[k]);
+    V[k] = v;
+    W[k] = (Real)((double)W[k] + (double)v);
+  }
+}
+
+template <typename Real>
+void alloc_state(const Net<Real>& net, BatchState<Real>& st, int64_t rows) {
+  st.a.assign(net.L + 1, {});
+  st.d.assign(net.L + 1, {});
+  for (int l = 0; l <= net.L; ++l) {
+    st.a[l].assign((size_t)(rows * net.n[l]), (Real)0);
+    if (l >= 1) st.d[l].assign((size_t)(rows * net.n[l]), (Real)0);
+  }
+  st.sse_p.assign((size_t)rows, 0.0);
+}
+
+// Input rows of patterns [p0, p0 + rows): dense copy or one-hot expansion.
+template <typename Real>
+void load_inputs(const Net<Real>& net, BatchState<Real>& st, int64_t p0, int64_t rows,
+                 const float* x, const int32_t* act, int n_active) {
+  const int n0 = net.n[0];
+  Real* a0 = st.a[0].data();
+  if (x) {
+    for (int64_t p = 0; p < rows; ++p)
+      for (int i = 0; i < n0; ++i) a0[p * n0 + i] = (Real)x[(p0 + p) * n0 + i];
+  } else {
+    std::memset(a0, 0, sizeof(Real) * (size_t)(rows * n0));
+    for (int64_t p = 0; p < rows; ++p)
+      for (int k = 0; k < n_active; ++k) a0[p * n0 + act[(p0 + p) * n_active + k]] = (Real)1;
+  }
+}
+
+// Checks one-hot indices: in range and distinct within each pattern.
+int check_active(const int32_t* act, int n_active, int64_t n, int n0) {
+  if (n > 0 && (!act || n_active < 1 || n_active > n0)) return -1;
+  for (int64_t p = 0; p < n; ++p) {
+    const int32_t* r = act + p * n_active;
+    for (int k = 0; k < n_active; ++k) {
+      if (r[k] < 0 || r[k] >= n0) return -1;
+      for (int q = 0; q < k; ++q)
+        if (r[q] == r[k]) return -1;
+    }
+  }
+  return 0;
+}
+
+template <typename Real>
+int train_epoch(Net<Real>& net, const float* x, const int32_t* act, int n_active, const float* t,
+                int64_t n, int32_t batch, double lr, double mom, double* sse, double* batch_sse) {
+  if (batch < 1 || n < 0 || (n > 0 && !t) || (n > 0 && !x && !act)) return -1;
+  if (!x && check_active(act, n_active, n, net.n[0])) return -1;
+  BatchState<Real> st;
+  alloc_state(net, st, std::min<int64_t>(batch, std::max<int64_t>(n, 1)));
+  std::vector<double> G((size_t)net.total);
+  double total = 0.0;
+  int64_t b = 0;
+  for (int64_t p0 = 0; p0 < n; p0 += batch, ++b) {
+    const int64_t rows = std::min<int64_t>(batch, n - p0);
+    load_inputs(net, st, p0, rows, x, act, n_active);
+    run_batch(net, st, rows, t + p0 * net.n[net.L]);
+    double bs = 0.0;
+    for (int64_t p = 0; p < rows; ++p) bs += st.sse_p[p];
+    batch_sum(net, st, rows, G.data());
+    apply_update(net, G.data(), lr, mom);
+    if (batch_sse) batch_sse[b] = bs;
+    total += bs;
+  }
+  if (sse) *sse = total;
+  return 0;
+}
+
+template <typename Real>
+int gradient(Net<Real>& net, const float* x, const int32_t* act, int n_active, const float* t,
+             int64_t n, double* G, double* sse) {
+  if (n < 1 || !t || !G || (!x && !act)) return -1;
+  if (!x && check_active(act, n_active, n, net.n[0])) return -1;
+  BatchState<Real> st;
+  alloc_state(net, st, n);
+  load_inputs(net, st, 0, n, x, act, n_active);
+  run_batch(net, st, n, t);
+  batch_sum(net, st, n, G);
+  if (sse) {
+    double s = 0.0;
+    for (int64_t p = 0; p < n; ++p) s += st.sse_p[p];
+    *sse = s;
+  }
+  return 0;
+}
+
+template <typename Real>
+int forward(Net<Real>& net, const float* x, const int32_t* act, int n_active, int64_t n, double* y) {
+  if (n < 0 || (n > 0 && (!y || (!x && !act)))) return -1;
+  if (!x && check_active(act, n_active, n, net.n[0])) return -1;
+  if (n == 0) return 0;
+  BatchState<Real> st;
+  alloc_state(net, st, n);
+  load_inputs(net, st, 0, n, x, act, n_active);
+  run_batch(net, st, n, nullptr);
+  const int nL = net.n[net.L];
+  for (int64_t k = 0; k < n * nL; ++k) y[k] = (double)st.a[net.L][k];
+  return 0;
+}
+
+// Activations a_1..a_L and deltas delta_1..delta_L of a batch at the current
+// weights, each layer as [n][n_l] (concatenated over l = 1..L).
+template <typename Real>
+int batch_state(Net<Real>& net, const float* x, const int32_t* act, int n_active, const float* t,
+                int64_t n, double* acts, double* deltas) {
+  if (n < 1 || !t || (!x && !act)) return -1;
+  if (!x && check_active(act, n_active, n, net.n[0])) return -1;
+  BatchState<Real> st;
+  alloc_state(net, st, n);
+  load_inputs(net, st, 0, n, x, act, n_active);
+  run_batch(net, st, n, t);
+  int64_t o = 0;
+  for (int l = 1; l <= net.L; ++l) {
+    for (int64_t k = 0; k < n * net.n[l]; ++k, ++o) {
+      if (acts) acts[o] = (double)st.a[l][k];
+      if (deltas) deltas[o] = (double)st.d[l][k];
+    }
+  }
+  return 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+struct orc_net {
+  int bits;             // 32 or 64: storage precision
+  Net<float> f;
+  Net<double> d;
+};
+
+static bool init_shape(std::vector<int>& n, std::vector<int64_t>& off, int64_t& total, int& L,
+                       const int32_t* sizes, int32_t n_sizes) {
+  if (!sizes || n_sizes < 2) return false;
+  L = n_sizes - 1;
+  n.assign(sizes, sizes + n_sizes);
+  for (int v : n)
+    if (v < 1) return false;
+  off.assign(L, 0);
+  total = 0;
+  for (int l = 0; l < L; ++l) {
+    off[l] = total;
+    total += (int64_t)(n[l] + 1) * n[l + 1];
+  }
+  return true;
+}
+
+orc_net* orc_create(const int32_t* sizes, int32_t n_sizes, int32_t storage_bits) {
+  if (storage_bits != 32 && storage_bits != 64) return nullptr;
+  orc_net* h = new orc_net();
+  h->bits = storage_bits;
+  bool ok = storage_bits == 32 ? init_shape(h->f.n, h->f.off, h->f.total, h->f.L, sizes, n_sizes)
+                               : init_shape(h->d.n, h->d.off, h->d.total, h->d.L, sizes, n_sizes);
+  if (!ok) {
+    delete h;
+    return nullptr;
+  }
+  if (storage_bits == 32) {
+    h->f.W.assign((size_t)h->f.total, 0.f);
+    h->f.V.assign((size_t)h->f.total, 0.f);
+  } else {
+    h->d.W.assign((size_t)h->d.total, 0.0);
+    h->d.V.assign((size_t)h->d.total, 0.0);
+  }
+  return h;
+}
+
+void orc_destroy(orc_net* h) { delete h; }
+
+int64_t orc_num_weights(const orc_net* h) { return h->bits == 32 ? h->f.total : h->d.total; }
+
+void orc_set_threads(int32_t n) {
+  if (n > 0) omp_set_num_threads(n);
+}
+
+int32_t orc_get_threads(void) { return omp_get_max_threads(); }
+
+#define ORC_DISPATCH(h, call) ((h)->bits == 32 ? call((h)->f) : call((h)->d))
+
+int orc_set_weights(orc_net* h, const double* w, int64_t n) {
+  if (!h || !w || n != orc_num_weights(h)) return -1;
+  auto set = [&](auto& net) {
+    using R = typename std::decay<decltype(net.W[0])>::type;
+    for (int64_t k = 0; k < n; ++k) {
+      net.W[k] = (R)w[k];
+      net.V[k] = (R)0;
+    }
+    return 0;
+  };
+  return ORC_DISPATCH(h, set);
+}
+
+int orc_get_weights(const orc_net* h, double* w, int64_t n) {
+  if (!h || !w || n != orc_num_weights(h)) return -1;
+  for (int64_t k = 0; k < n; ++k) w[k] = h->bits == 32 ? (double)h->f.W[k] : h->d.W[k];
+  return 0;
+}
+
+int orc_set_momentum(orc_net* h, const double* v, int64_t n) {
+  if (!h || !v || n != orc_num_weights(h)) return -1;
+  for (int64_t k = 0; k < n; ++k) {
+    if (h->bits == 32) h->f.V[k] = (float)v[k];
+    else h->d.V[k] = v[k];
+  }
+  return 0;
+}
+
+int orc_get_momentum(const orc_net* h, double* v, int64_t n) {
+  if (!h || !v || n != orc_num_weights(h)) return -1;
+  for (int64_t k = 0; k < n; ++k) v[k] = h->bits == 32 ? (double)h->f.V[k] : h->d.V[k];
+  return 0;
+}
+
+int orc_forward(orc_net* h, const float* x, int64_t n, double* y) {
+  if (!h || (n > 0 && !x)) return -1;
+  auto f = [&](auto& net) { return forward(net, x, nullptr, 0, n, y); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_forward_onehot(orc_net* h, const int32_t* act, int32_t n_active, int64_t n, double* y) {
+  if (!h || (n > 0 && !act)) return -1;
+  auto f = [&](auto& net) { return forward(net, (const float*)nullptr, act, n_active, n, y); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_gradient(orc_net* h, const float* x, const float* t, int64_t n, double* G, double* sse) {
+  if (!h || !x) return -1;
+  auto f = [&](auto& net) { return gradient(net, x, nullptr, 0, t, n, G, sse); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_gradient_onehot(orc_net* h, const int32_t* act, int32_t n_active, const float* t, int64_t n,
+                        double* G, double* sse) {
+  if (!h || !act) return -1;
+  auto f = [&](auto& net) { return gradient(net, (const float*)nullptr, act, n_active, t, n, G, sse); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_batch_state(orc_net* h, const float* x, const float* t, int64_t n, double* acts, double* deltas) {
+  if (!h || !x) return -1;
+  auto f = [&](auto& net) { return batch_state(net, x, nullptr, 0, t, n, acts, deltas); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_train_epoch(orc_net* h, const float* x, const float* t, int64_t n, int32_t batch, double lr,
+                    double mom, double* sse, double* batch_sse) {
+  if (!h || (n > 0 && !x)) return -1;
+  auto f = [&](auto& net) { return train_epoch(net, x, nullptr, 0, t, n, batch, lr, mom, sse, batch_sse); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_train_epoch_onehot(orc_net* h, const int32_t* act, int32_t n_active, const float* t, int64_t n,
+                           int32_t batch, double lr, double mom, double* sse, double* batch_sse) {
+  if (!h || (n > 0 && !act)) return -1;
+  auto f = [&](auto& net) {
+    return train_epoch(net, (const float*)nullptr, act, n_active, t, n, batch, lr, mom, sse, batch_sse);
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+}  // extern "C"
