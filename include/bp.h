@@ -1,0 +1,133 @@
+/*
+ * bp.h -- C-ABI of libbp.so: pooled back-propagation for fully connected
+ * sigmoid nets, fp32, on one MI355X (gfx950).
+ *
+ * The method (Witbrock & Zagha, "An Implementation of Back-Propagation
+ * Learning on GF11", CMU-CS-89-208):
+ *   - forward: each unit takes the weighted sum of the units feeding it plus
+ *     the weight from the always-on "true unit", then the logistic
+ *     1/(1+e^-x) (section 3 and footnote 4; true unit: section 6.3);
+ *   - error: summed squared difference of targets and outputs (section 3
+ *     footnote 5, section 8);
+ *   - backward: deltas from the output layer back to the first hidden layer;
+ *     the input layer gets none (section 3; the cycle counts of section 6.1);
+ *   - pooled update: the weight changes of all patterns of a batch are summed
+ *     and applied once, with learning rate and momentum (sections 3, 4.1,
+ *     6.2.1 and 9):  V = lr * G + momentum * V;  W += V,
+ *     G[i][j] = sum over the batch of a_l[i] * delta_{l+1}[j].
+ *
+ * Layer sizes n_0 .. n_L (n_layers = L + 1 >= 2 entries).  Weight layout for
+ * bp_set_weights / bp_get_weights / bp_*_momentum: the concatenation over
+ * l = 0 .. L-1 of W_l, each (n_l + 1) x n_{l+1} row-major, row i = input unit
+ * i, last row = the true unit (bias).  Its length is the paper's connection
+ * count, sum (n_l + 1) * n_{l+1} (13,826 for the 203-60-26 NETtalk net).
+ *
+ * Ownership: the net owns its weights, momentum and workspace (device
+ * memory).  Callers own every buffer they pass; "_dev" pointers are device
+ * memory, contiguous row-major; "_host" pointers are host memory.
+ *
+ * Errors: every entry point returns BP_OK or a negative code; nothing throws
+ * across this boundary.  Arguments are checked on the host before any device
+ * work, so a BP_EINVAL return leaves the net unchanged.  BP_EDEVICE reports a
+ * HIP runtime error; weights and momentum are then undefined until the next
+ * bp_set_weights.  bp_last_error gives the message of the last failure.
+ *
+ * Streams: work is enqueued on the net's stream (bp_set_stream; default: the
+ * null stream).  Train and forward calls return once the work is enqueued,
+ * except that a non-NULL sse_out waits for the result.  A net is not
+ * thread-safe; distinct nets are independent.
+ */
+#ifndef BP_H
+#define BP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct bp_net bp_net;
+
+enum {
+  BP_OK = 0,
+  BP_EINVAL = -1,   /* bad argument; nothing was done */
+  BP_ENOMEM = -2,   /* device allocation failed */
+  BP_EDEVICE = -3   /* HIP runtime error */
+};
+
+/* Creates a net with layer sizes layer_sizes[0 .. n_layers-1] (each >= 1,
+ * n_layers >= 2) on the current HIP device.  Weights and momentum start at
+ * zero.  *out receives the handle (NULL on failure). */
+int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out);
+
+/* Frees the net and its device memory after its stream has drained.  NULL is a no-op. */
+void bp_destroy(bp_net* net);
+
+/* Sets the HIP stream (a hipStream_t, e.g. torch.cuda.current_stream().cuda_stream)
+ * all later work of this net is enqueued on.  NULL selects the null stream. */
+int bp_set_stream(bp_net* net, void* hip_stream);
+
+/* Number of weights = connections, bias rows included (section 6.3, section 7.1).
+ * Returns -1 for a NULL net. */
+int64_t bp_num_weights(const bp_net* net);
+
+/* Copies n == bp_num_weights weights from host memory (layout above) and
+ * zeroes the momentum.  Synchronous. */
+int bp_set_weights(bp_net* net, const float* w_host, int64_t n);
+
+/* Copies the n == bp_num_weights current weights to host memory.  Waits for
+ * the net's stream.  Synchronous. */
+int bp_get_weights(bp_net* net, float* w_host, int64_t n);
+
+/* Momentum state V (the previous change, sections 6.2.1 and 9), same layout
+ * as the weights.  Needed for an exact resume.  Synchronous. */
+int bp_set_momentum(bp_net* net, const float* v_host, int64_t n);
+int bp_get_momentum(bp_net* net, float* v_host, int64_t n);
+
+/* One pass (epoch) over n_patterns dense patterns, in order, with one pooled
+ * update per `batch` patterns (ceil(n_patterns / batch) updates; a short last
+ * batch is applied like the others).  Momentum persists across batches and
+ * calls.
+ *   inputs_dev  : float [n_patterns][n_0]
+ *   targets_dev : float [n_patterns][n_L]
+ *   batch >= 1; lr and momentum are used exactly as given (the change is the
+ *   SUM over the batch; pass lr / batch for a mean).
+ *   sse_out     : if non-NULL, receives the summed squared error of the epoch,
+ *                 each pattern measured with the weights of its own batch's
+ *                 forward pass; the call then waits for the stream.
+ * Returns BP_EINVAL for NULL pointers (n_patterns > 0), n_patterns < 0 or
+ * batch < 1. */
+int bp_train_batches(bp_net* net, const float* inputs_dev, const float* targets_dev, int64_t n_patterns,
+                     int32_t batch, float lr, float momentum, double* sse_out);
+
+/* As bp_train_batches, for inputs that are 0/1 with exactly n_active ones per
+ * pattern (the NETtalk window coding: 7 positions x 29 symbols, section 6.3),
+ * given as the indices of the ones:
+ *   active_dev : int32 [n_patterns][n_active], each in [0, n_0), distinct
+ *                within a pattern (not checked on the device: out-of-range
+ *                indices are undefined behaviour).
+ * The first layer gathers the n_active weight rows instead of multiplying;
+ * its change touches only those rows, while the momentum term still moves
+ * every row.  1 <= n_active <= n_0. */
+int bp_train_batches_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active,
+                            const float* targets_dev, int64_t n_patterns, int32_t batch, float lr,
+                            float momentum, double* sse_out);
+
+/* Forward pass only (no update): outputs_dev float [n_patterns][n_L] receives
+ * the output activations for inputs_dev float [n_patterns][n_0]. */
+int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* outputs_dev);
+
+/* Forward pass only for one-hot inputs given as active indices (see
+ * bp_train_batches_onehot). */
+int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, int64_t n_patterns,
+                      float* outputs_dev);
+
+/* Message describing the last non-OK return on this net (or of bp_create
+ * when net is NULL).  Valid until the next call on the net. */
+const char* bp_last_error(const bp_net* net);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BP_H */

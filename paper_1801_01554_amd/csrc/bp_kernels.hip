@@ -1,0 +1,570 @@
+// bp_kernels.hip -- gfx950 (CDNA4) kernels of pooled back-propagation, fp32.
+//
+// The three weight contractions of one pooled update (forward, hidden deltas,
+// summed change) are dense fp32 products and run on the matrix cores
+// (v_mfma_f32_32x32x2_f32) with LDS-staged tiles; each one fuses the
+// elementwise step that follows it in the method:
+//   forward     A_{l+1} = sigma(A_l W_l + bias)             (section 3)
+//   output      delta_L = (T - Y) Y (1 - Y), error partials  (section 3, fn 5)
+//   backward    delta_l = (delta_{l+1} W_l^T) * A_l (1 - A_l) (section 3)
+//   change      V = lr (A_l^T delta_{l+1}) + mom V; W += V    (sections 3, 6.2.1)
+// The one-hot first layer of the NETtalk-style input window (section 6.3)
+// gathers and scatters weight rows instead of multiplying by a 0/1 matrix.
+//
+// Every reduction runs in a fixed order: results are run-to-run identical.
+#include <hip/hip_runtime.h>
+
+#include "bp_internal.h"
+
+namespace bpk {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
+
+// --------------------------------------------------------------------------
+// Epilogues.  apply() gets one element of the product (row m, column n) plus
+// the per-column value column() returned; kSSE marks epilogues that add to a
+// per-block squared-error partial.
+
+struct EpiSigmoid {
+  const float* bias;
+  float* out;
+  int ldo;
+  static constexpr bool kSSE = false;
+  __device__ float column(int n) const { return bias[n]; }
+  __device__ void apply(int m, int n, float acc, float b, float&) const {
+    out[(size_t)m * ldo + n] = logistic(acc + b);
+  }
+};
+
+struct EpiOutputDelta {
+  const float* bias;
+  const float* T;
+  int ldt;
+  float* delta;
+  int ldd;
+  double* sse_part;
+  static constexpr bool kSSE = true;
+  __device__ float column(int n) const { return bias[n]; }
+  __device__ void apply(int m, int n, float acc, float b, float& sse) const {
+    const float y = logistic(acc + b);
+    const float e = T[(size_t)m * ldt + n] - y;
+    sse += e * e;
+    delta[(size_t)m * ldd + n] = e * y * (1.0f - y);
+  }
+};
+
+struct EpiHiddenDelta {
+  const float* act;
+  int lda;
+  float* out;
+  int ldo;
+  static constexpr bool kSSE = false;
+  __device__ float column(int) const { return 0.f; }
+  __device__ void apply(int m, int n, float acc, float, float&) const {
+    const float a = act[(size_t)m * lda + n];
+    out[(size_t)m * ldo + n] = acc * (a * (1.0f - a));
+  }
+};
+
+struct EpiUpdate {
+  float* W;
+  float* V;
+  int ldw;
+  float lr, mom;
+  static constexpr bool kSSE = false;
+  __device__ float column(int) const { return 0.f; }
+  __device__ void apply(int m, int n, float acc, float, float&) const {
+    const size_t i = (size_t)m * ldw + n;
+    const float v = lr * acc + mom * V[i];
+    V[i] = v;
+    W[i] = W[i] + v;
+  }
+};
+
+// Split-K partial: P[z][m][n] for z = blockIdx.z.
+struct EpiPartial {
+  float* P;
+  int ldp;
+  size_t split_stride;
+  static constexpr bool kSSE = false;
+  __device__ float column(int) const { return 0.f; }
+  __device__ void apply(int m, int n, float acc, float, float&) const {
+    P[blockIdx.z * split_stride + (size_t)m * ldp + n] = acc;
+  }
+};
+
+// --------------------------------------------------------------------------
+// Tiled fp32 MFMA product C[M][N] = sum_k A(m, k) B(k, n).
+//
+// Operand storage (global and LDS alike, so tiles are copied without a
+// transpose):  A_KM false: A[m * lda + k]   true: A[k * lda + m]
+//              B_NK false: B[k * ldb + n]   true: B[n * ldb + k]
+// 256 threads = 4 waves in a 2 x 2 grid; each wave owns a (BM/2) x (BN/2)
+// sub-tile made of 32 x 32 MFMA blocks.  Within a group of 8 k values, MFMA
+// t (t = 0..3) pairs k = 8g + t (lanes 0-31) with k = 8g + 4 + t (lanes
+// 32-63); A and B use the same assignment, so each lane can fetch its four k
+// values of a k-contiguous tile with one 16-byte LDS read.
+template <int BM, int BN, int BK, bool A_KM, bool B_NK>
+struct Tile {
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr int SA = A_KM ? (BM + 8) : (BK + 4);   // LDS row strides (floats)
+  static constexpr int SB = B_NK ? (BK + 4) : (BN + 8);
+  static constexpr int A_ELEMS = A_KM ? BK * SA : BM * SA;
+  static constexpr int B_ELEMS = B_NK ? BN * SB : BK * SB;
+  static constexpr int LA = BM * BK / 4 / kThreads;        // float4 loads per thread per stage
+  static constexpr int LB = BN * BK / 4 / kThreads;
+  static_assert(BM % 64 == 0 && BN % 64 == 0 && BK % 8 == 0, "tile shape");
+  static_assert(LA * 4 * kThreads == BM * BK && LB * 4 * kThreads == BN * BK, "tile split");
+};
+
+// Loads a TO x TD tile (TD contiguous) whose origin is (o0, d0) into
+// registers; elements outside [0, O_lim) x [0, D_lim) read as zero.
+template <int TO, int TD, bool VEC>
+__device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld, int o0, int d0, int O_lim,
+                                          int D_lim, f32x4* r) {
+  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int D4 = TD / 4;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int f = threadIdx.x + q * kThreads;
+    const int go = o0 + f / D4, gd = d0 + (f % D4) * 4;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (go < O_lim) {
+      const float* p = base + (size_t)go * ld + gd;
+      if (VEC && gd + 4 <= D_lim) {
+        v = *reinterpret_cast<const f32x4*>(p);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (gd + e < D_lim) v[e] = p[e];
+      }
+    }
+    r[q] = v;
+  }
+}
+
+template <int TO, int TD, int S>
+__device__ __forceinline__ void store_tile(float* lds, const f32x4* r) {
+  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int D4 = TD / 4;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int f = threadIdx.x + q * kThreads;
+    *reinterpret_cast<f32x4*>(lds + (f / D4) * S + (f % D4) * 4) = r[q];
+  }
+}
+
+// Maps the hardware block index to a tile so that the blocks one XCD receives
+// (hardware index mod 8) are consecutive tiles of the same tile row: they
+// share their A tiles in that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
+  const int per = nblocks >> 3;
+  if (bid >= (per << 3)) return bid;
+  return (bid & 7) * per + (bid >> 3);
+}
+
+template <int BM, int BN, int BK, bool A_KM, bool B_NK, bool AVEC, bool BVEC, class Epi>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict__ A, int lda,
+                                                        const float* __restrict__ B, int ldb, int M, int N,
+                                                        int K, int k_chunk, Epi epi) {
+  using T = Tile<BM, BN, BK, A_KM, B_NK>;
+  __shared__ __attribute__((aligned(16))) float As[2][T::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) float Bs[2][T::B_ELEMS];
+
+  const int tiles_n = (N + BN - 1) / BN;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int kb = blockIdx.z * k_chunk;
+  const int ke = min(K, kb + k_chunk);
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm0 = (wave >> 1) * T::WM, wn0 = (wave & 1) * T::WN;
+  const int r = lane & 31, h = lane >> 5;
+
+  f32x16 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  f32x4 ra[T::LA], rb[T::LB];
+  auto load_stage = [&](int k) {
+    if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra);
+    else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra);
+    if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb);
+    else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb);
+  };
+  auto store_stage = [&](int buf) {
+    if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra);
+    else store_tile<BM, BK, T::SA>(As[buf], ra);
+    if (B_NK) store_tile<BN, BK, T::SB>(Bs[buf], rb);
+    else store_tile<BK, BN, T::SB>(Bs[buf], rb);
+  };
+
+  const int nst = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+  if (nst > 0) {
+    load_stage(kb);
+    store_stage(0);
+    __syncthreads();
+  }
+  for (int s = 0; s < nst; ++s) {
+    const int cur = s & 1;
+    if (s + 1 < nst) load_stage(kb + (s + 1) * BK);
+    const float* as = As[cur];
+    const float* bs = Bs[cur];
+#pragma unroll
+    for (int g = 0; g < BK / 8; ++g) {
+      f32x4 af[T::TM], bf[T::TN];
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i) {
+        const int m = wm0 + i * 32 + r;
+        if (A_KM) {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) af[i][t] = as[(g * 8 + 4 * h + t) * T::SA + m];
+        } else {
+          af[i] = *reinterpret_cast<const f32x4*>(as + m * T::SA + g * 8 + 4 * h);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int n = wn0 + j * 32 + r;
+        if (B_NK) {
+          bf[j] = *reinterpret_cast<const f32x4*>(bs + n * T::SB + g * 8 + 4 * h);
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) bf[j][t] = bs[(g * 8 + 4 * h + t) * T::SB + n];
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+          for (int j = 0; j < T::TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][t], bf[j][t], acc[i][j], 0, 0, 0);
+    }
+    if (s + 1 < nst) store_stage(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
+  // row 8 (e / 4) + 4 h + (e % 4), column r.
+  float sse = 0.f;
+#pragma unroll
+  for (int j = 0; j < T::TN; ++j) {
+    const int n = n0 + wn0 + j * 32 + r;
+    if (n < N) {
+      const float cv = epi.column(n);
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+          if (m < M) epi.apply(m, n, acc[i][j][e], cv, sse);
+        }
+      }
+    }
+  }
+  if constexpr (Epi::kSSE) {
+    __shared__ float red[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+    if (lane == 0) red[wave] = sse;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double s = 0.0;
+      for (int w = 0; w < kThreads / 64; ++w) s += (double)red[w];
+      epi.sse_part[blockIdx.x] = s;
+    }
+  }
+}
+
+// Tile configurations.
+constexpr int BK = 32;
+
+template <int BM, int BN, bool A_KM, bool B_NK, class Epi>
+hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
+                       int splits, int k_chunk, const Epi& epi) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const bool avec = (lda % 4 == 0) && ((reinterpret_cast<uintptr_t>(A) & 15) == 0);
+  const bool bvec = (ldb % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) & 15) == 0);
+  dim3 grid(tiles, 1, splits), block(kThreads);
+  if (avec && bvec)
+    gemm_kernel<BM, BN, BK, A_KM, B_NK, true, true, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
+  else if (avec)
+    gemm_kernel<BM, BN, BK, A_KM, B_NK, true, false, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
+  else if (bvec)
+    gemm_kernel<BM, BN, BK, A_KM, B_NK, false, true, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
+  else
+    gemm_kernel<BM, BN, BK, A_KM, B_NK, false, false, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
+  return hipGetLastError();
+}
+
+constexpr int kBM = 128, kBN = 128;
+
+// --------------------------------------------------------------------------
+// Split-K reduction of the change followed by the momentum update.
+__global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __restrict__ P, int splits,
+                                                                 size_t split_stride, int M, int N, int ldp,
+                                                                 float* W, float* V, int ldw, float lr,
+                                                                 float mom) {
+  const size_t idx = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (size_t)M * N) return;
+  const int m = (int)(idx / N), n = (int)(idx % N);
+  float g = 0.f;
+  for (int z = 0; z < splits; ++z) g += P[z * split_stride + (size_t)m * ldp + n];
+  const size_t i = (size_t)m * ldw + n;
+  const float v = lr * g + mom * V[i];
+  V[i] = v;
+  W[i] = W[i] + v;
+}
+
+// Bias-row change: column sums of D over `rows` rows, then the update.  Block
+// = 1024 threads = 16 waves; lane = column within a 64-column strip; wave w
+// sums its contiguous share of the rows in order, then the 16 partial sums
+// are added in wave order.
+constexpr int kBiasWaves = 16;
+__global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(const float* __restrict__ D, int ldd,
+                                                                       int rows, int N, float* Wb, float* Vb,
+                                                                       float lr, float mom) {
+  __shared__ float part[kBiasWaves][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 64 + lane;
+  const int r0 = (int)((int64_t)rows * wave / kBiasWaves), r1 = (int)((int64_t)rows * (wave + 1) / kBiasWaves);
+  float s = 0.f;
+  if (n < N) {
+    int k = r0;
+    for (; k + 4 <= r1; k += 4) {
+      const float a0 = D[(size_t)k * ldd + n], a1 = D[(size_t)(k + 1) * ldd + n];
+      const float a2 = D[(size_t)(k + 2) * ldd + n], a3 = D[(size_t)(k + 3) * ldd + n];
+      s += a0;
+      s += a1;
+      s += a2;
+      s += a3;
+    }
+    for (; k < r1; ++k) s += D[(size_t)k * ldd + n];
+  }
+  part[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && n < N) {
+    float g = 0.f;
+    for (int w = 0; w < kBiasWaves; ++w) g += part[w][lane];
+    const float v = lr * g + mom * Vb[n];
+    Vb[n] = v;
+    Wb[n] = Wb[n] + v;
+  }
+}
+
+// One-hot first layer forward.  One wave per (pattern, 64-column strip).
+__global__ __launch_bounds__(kThreads) void onehot_forward_kernel(const int32_t* __restrict__ act, int n_active,
+                                                                  int rows, const float* __restrict__ W0, int ldw,
+                                                                  int n0, int H, int strips, int mode, float* out,
+                                                                  int ldo, const float* __restrict__ T, int ldt,
+                                                                  double* sse_part) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int item = blockIdx.x * (kThreads / 64) + wave;
+  const int p = item / strips, col = (item % strips) * 64 + lane;
+  float sse = 0.f;
+  if (p < rows && col < H) {
+    float net = W0[(size_t)n0 * ldw + col];
+    const int32_t* a = act + (size_t)p * n_active;
+    for (int k = 0; k < n_active; ++k) net += W0[(size_t)a[k] * ldw + col];
+    const float y = logistic(net);
+    if (mode == 0) {
+      out[(size_t)p * ldo + col] = y;
+    } else {
+      const float e = T[(size_t)p * ldt + col] - y;
+      sse = e * e;
+      out[(size_t)p * ldo + col] = e * y * (1.0f - y);
+    }
+  }
+  if (mode == 1) {
+    __shared__ float red[kThreads / 64];
+    for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+    if (lane == 0) red[wave] = sse;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double s = 0.0;
+      for (int w = 0; w < kThreads / 64; ++w) s += (double)red[w];
+      sse_part[blockIdx.x] = s;
+    }
+  }
+}
+
+// One-hot first-layer change + update.  Block (r, c): weight row r (r == n0 is
+// the bias row) and columns [256 c, 256 c + 256).  The patterns containing
+// index r are listed in pattern order (ballot compaction, 256 patterns at a
+// time) and their delta rows summed in that order.
+__global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* __restrict__ act, int n_active,
+                                                                 int rows, const float* __restrict__ D, int ldd,
+                                                                 int n0, int H, float* W, float* V, int ldw,
+                                                                 float lr, float mom) {
+  __shared__ int list[kThreads];
+  __shared__ int wave_cnt[kThreads / 64];
+  const int r = blockIdx.x;
+  const int col = blockIdx.y * kThreads + threadIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float g = 0.f;
+  for (int p0 = 0; p0 < rows; p0 += kThreads) {
+    const int p = p0 + threadIdx.x;
+    bool hit = false;
+    if (p < rows) {
+      if (r == n0) {
+        hit = true;
+      } else {
+        const int32_t* a = act + (size_t)p * n_active;
+        for (int k = 0; k < n_active; ++k) hit |= (a[k] == r);
+      }
+    }
+    const unsigned long long bal = __ballot(hit);
+    if (lane == 0) wave_cnt[wave] = __popcll(bal);
+    __syncthreads();
+    int base = 0, total = 0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      if (w < wave) base += wave_cnt[w];
+      total += wave_cnt[w];
+    }
+    if (hit) {
+      const unsigned long long below = lane ? (bal & ((1ull << lane) - 1ull)) : 0ull;
+      list[base + __popcll(below)] = p;
+    }
+    __syncthreads();
+    if (col < H)
+      for (int q = 0; q < total; ++q) g += D[(size_t)list[q] * ldd + col];
+    __syncthreads();
+  }
+  if (col < H) {
+    const size_t i = (size_t)r * ldw + col;
+    const float v = lr * g + mom * V[i];
+    V[i] = v;
+    W[i] = W[i] + v;
+  }
+}
+
+// Fixed-order sum of n doubles by one block.
+__global__ __launch_bounds__(kThreads) void sse_reduce_kernel(const double* __restrict__ part, int n,
+                                                              double* out) {
+  __shared__ double red[kThreads];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < n; i += kThreads) s += part[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = kThreads / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
+int choose_splits(int M, int N, int K) {
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  if (K < 1024 || tiles >= 128) return 1;
+  int s = (256 + tiles - 1) / tiles;
+  const int max_s = K / 256;
+  if (s > max_s) s = max_s;
+  return s < 1 ? 1 : s;
+}
+
+int chunk_for(int K, int splits) {
+  int c = (K + splits - 1) / splits;
+  return (c + BK - 1) / BK * BK;
+}
+
+}  // namespace
+
+// --------------------------------------------------------------------------
+// Launch wrappers (declared in bp_internal.h).
+
+int output_delta_blocks(int M, int N) { return ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN); }
+
+hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
+                         const float* bias, float* out, int ldo) {
+  EpiSigmoid e{bias, out, ldo};
+  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+}
+
+hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
+                                int K, const float* bias, const float* T, int ldt, float* delta, int ldd,
+                                double* sse_part) {
+  EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part};
+  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+}
+
+hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,
+                          const float* act, int lda, float* out, int ldo) {
+  EpiHiddenDelta e{act, lda, out, ldo};
+  return launch_gemm<kBM, kBN, false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
+}
+
+size_t change_update_workspace(int M, int N, int K) {
+  const int sp = choose_splits(M, N, K);
+  if (sp <= 1) return 0;
+  const int ldp = (N + 3) / 4 * 4;
+  return (size_t)sp * M * ldp;
+}
+
+hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N, int K,
+                         float* W, float* V, int ldw, float lr, float mom, float* ws) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const int sp = choose_splits(M, N, K);
+  if (sp <= 1) {
+    EpiUpdate e{W, V, ldw, lr, mom};
+    return launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
+  }
+  const int ldp = (N + 3) / 4 * 4;
+  const size_t stride = (size_t)M * ldp;
+  EpiPartial e{ws, ldp, stride};
+  hipError_t err = launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
+  if (err != hipSuccess) return err;
+  const size_t total = (size_t)M * N;
+  splitk_update_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(ws, sp, stride, M, N, ldp,
+                                                                                         W, V, ldw, lr, mom);
+  return hipGetLastError();
+}
+
+hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb, float lr,
+                       float mom) {
+  if (N <= 0) return hipSuccess;
+  bias_update_kernel<<<(N + 63) / 64, 64 * kBiasWaves, 0, s>>>(D, ldd, rows, N, Wb, Vb, lr, mom);
+  return hipGetLastError();
+}
+
+int onehot_forward_blocks(int rows, int H) {
+  const int strips = (H + 63) / 64;
+  const long items = (long)rows * strips;
+  return (int)((items + 3) / 4);
+}
+
+hipError_t onehot_forward(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw,
+                          int n0, int H, int mode, float* out, int ldo, const float* T, int ldt, double* sse_part) {
+  if (rows <= 0 || H <= 0) return hipSuccess;
+  const int strips = (H + 63) / 64;
+  onehot_forward_kernel<<<onehot_forward_blocks(rows, H), kThreads, 0, s>>>(act, n_active, rows, W0, ldw, n0, H,
+                                                                            strips, mode, out, ldo, T, ldt, sse_part);
+  return hipGetLastError();
+}
+
+hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* D, int ldd, int n0,
+                         int H, float* W, float* V, int ldw, float lr, float mom) {
+  if (H <= 0) return hipSuccess;
+  dim3 grid(n0 + 1, (H + kThreads - 1) / kThreads);
+  onehot_update_kernel<<<grid, kThreads, 0, s>>>(act, n_active, rows, D, ldd, n0, H, W, V, ldw, lr, mom);
+  return hipGetLastError();
+}
+
+hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out) {
+  sse_reduce_kernel<<<1, kThreads, 0, s>>>(part, n, out);
+  return hipGetLastError();
+}
+
+}  // namespace bpk

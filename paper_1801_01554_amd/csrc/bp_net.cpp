@@ -1,0 +1,432 @@
+// bp_net.cpp -- host side of the C-ABI in include/bp.h.
+//
+// Owns the device state of a net (weights W, momentum V, workspace), checks
+// every argument before any device work, and enqueues the launch sequence of
+// one pooled update per batch (sections 3 and 4.1 of the paper):
+//   forward l = 0 .. L-1  ->  output deltas + error partials
+//   for l = L-1 .. 1:  hidden deltas of layer l (with the pre-update W_l),
+//                      then the change and update of W_l
+//   change and update of W_0 (dense product, or the one-hot row scatter).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "bp.h"
+#include "bp_internal.h"
+
+struct bp_net {
+  int L = 0;                          // weight layers
+  std::vector<int> n;                 // n[0..L]
+  std::vector<int> ldw;               // padded row length of W_l (floats)
+  std::vector<int> lda;               // padded row length of activations/deltas of layer l
+  std::vector<int64_t> woff;          // device offset of W_l (floats)
+  std::vector<int64_t> foff;          // offset of W_l in the flat ABI layout
+  int64_t wtotal = 0;                 // device floats of W (padding included)
+  int64_t nweights = 0;               // connection count
+  float* W = nullptr;
+  float* V = nullptr;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  // workspace
+  int64_t ws_rows = 0;
+  std::vector<float*> act;            // act[l], l = 1 .. L-1 : [ws_rows][lda[l]]
+  std::vector<float*> del;            // del[l], l = 1 .. L   : [ws_rows][lda[l]]
+  float* fwd_tmp[2] = {nullptr, nullptr};  // forward-only ping-pong buffers
+  int64_t fwd_rows = 0;
+  size_t fwd_cap = 0;
+  float* splitk = nullptr;
+  size_t splitk_cap = 0;
+  double* sse_part = nullptr;
+  size_t sse_cap = 0;
+  double* sse_dev = nullptr;
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_create_err;
+
+int fail(bp_net* net, int code, const std::string& msg) {
+  if (net) net->err = msg;
+  else g_create_err = msg;
+  return code;
+}
+
+int hip_fail(bp_net* net, hipError_t e, const char* what) {
+  char buf[256];
+  std::snprintf(buf, sizeof(buf), "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+  return fail(net, e == hipErrorOutOfMemory ? BP_ENOMEM : BP_EDEVICE, buf);
+}
+
+#define BP_HIP(net, expr)                                   \
+  do {                                                      \
+    hipError_t e_ = (expr);                                 \
+    if (e_ != hipSuccess) return hip_fail((net), e_, #expr); \
+  } while (0)
+
+int round4(int v) { return (v + 3) / 4 * 4; }
+
+void free_ptr(void* p) {
+  if (p) (void)hipFree(p);
+}
+
+void free_workspace(bp_net* net) {
+  for (float* p : net->act) free_ptr(p);
+  for (float* p : net->del) free_ptr(p);
+  net->act.assign(net->L + 1, nullptr);
+  net->del.assign(net->L + 1, nullptr);
+  net->ws_rows = 0;
+  free_ptr(net->splitk);
+  net->splitk = nullptr;
+  net->splitk_cap = 0;
+}
+
+int ensure_workspace(bp_net* net, int64_t rows) {
+  if (rows <= net->ws_rows) return BP_OK;
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  free_workspace(net);
+  for (int l = 1; l <= net->L; ++l) {
+    const size_t bytes = sizeof(float) * (size_t)rows * net->lda[l];
+    if (l < net->L) BP_HIP(net, hipMalloc(&net->act[l], bytes));
+    BP_HIP(net, hipMalloc(&net->del[l], bytes));
+  }
+  size_t sk = 0;
+  for (int l = 0; l < net->L; ++l)
+    sk = std::max(sk, bpk::change_update_workspace(net->n[l], net->n[l + 1], (int)rows));
+  if (sk) BP_HIP(net, hipMalloc(&net->splitk, sizeof(float) * sk));
+  net->splitk_cap = sk;
+  net->ws_rows = rows;
+  return BP_OK;
+}
+
+int ensure_sse(bp_net* net, size_t count) {
+  if (!net->sse_dev) BP_HIP(net, hipMalloc(&net->sse_dev, sizeof(double)));
+  if (count <= net->sse_cap) return BP_OK;
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  free_ptr(net->sse_part);
+  net->sse_part = nullptr;
+  net->sse_cap = 0;
+  BP_HIP(net, hipMalloc(&net->sse_part, sizeof(double) * count));
+  net->sse_cap = count;
+  return BP_OK;
+}
+
+bool aligned_ptr(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+float* wl(bp_net* net, int l) { return net->W + net->woff[l]; }
+float* vl(bp_net* net, int l) { return net->V + net->woff[l]; }
+float* wbias(bp_net* net, int l) { return wl(net, l) + (size_t)net->n[l] * net->ldw[l]; }
+float* vbias(bp_net* net, int l) { return vl(net, l) + (size_t)net->n[l] * net->ldw[l]; }
+
+// Copies between the flat ABI layout (host) and the padded device layout.
+int copy_layers(bp_net* net, float* dev, const float* host_src, float* host_dst) {
+  for (int l = 0; l < net->L; ++l) {
+    const size_t rows = (size_t)net->n[l] + 1, cols = (size_t)net->n[l + 1];
+    float* d = dev + net->woff[l];
+    if (host_src)
+      BP_HIP(net, hipMemcpy2DAsync(d, sizeof(float) * net->ldw[l], host_src + net->foff[l], sizeof(float) * cols,
+                                   sizeof(float) * cols, rows, hipMemcpyHostToDevice, net->stream));
+    else
+      BP_HIP(net, hipMemcpy2DAsync(host_dst + net->foff[l], sizeof(float) * cols, d, sizeof(float) * net->ldw[l],
+                                   sizeof(float) * cols, rows, hipMemcpyDeviceToHost, net->stream));
+  }
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  return BP_OK;
+}
+
+// Inputs of one batch: dense rows or one-hot index rows.
+struct BatchInput {
+  const float* x = nullptr;       // dense [rows][n0]
+  const int32_t* act = nullptr;   // one-hot [rows][n_active]
+  int n_active = 0;
+};
+
+// Forward pass of `rows` patterns; the last layer either applies the output
+// delta epilogue (training, T != nullptr) or writes sigma to `out`.
+int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part,
+                float* out, int ldo, float* const* acts) {
+  const int L = net->L;
+  hipStream_t s = net->stream;
+  for (int l = 0; l < L; ++l) {
+    const bool last = (l == L - 1);
+    float* dst = last ? (T ? net->del[L] : out) : acts[l + 1];
+    const int ldd = last ? (T ? net->lda[L] : ldo) : net->lda[l + 1];
+    if (l == 0 && in.act) {
+      BP_HIP(net, bpk::onehot_forward(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], net->n[0], net->n[1],
+                                      (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part));
+      continue;
+    }
+    const float* A = (l == 0) ? in.x : acts[l];
+    const int ldA = (l == 0) ? net->n[0] : net->lda[l];
+    if (last && T)
+      BP_HIP(net, bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
+                                            wbias(net, l), T, net->n[L], dst, ldd, sse_part));
+    else
+      BP_HIP(net, bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
+                                     wbias(net, l), dst, ldd));
+  }
+  return BP_OK;
+}
+
+int sse_blocks(const bp_net* net, const BatchInput& in, int rows) {
+  if (net->L == 1 && in.act) return bpk::onehot_forward_blocks(rows, net->n[1]);
+  return bpk::output_delta_blocks(rows, net->n[net->L]);
+}
+
+// Backward pass and update of one batch whose deltas of the output layer are
+// in del[L].
+int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, float mom) {
+  hipStream_t s = net->stream;
+  for (int l = net->L - 1; l >= 0; --l) {
+    // Hidden deltas of layer l use W_l before its update.
+    if (l >= 1)
+      BP_HIP(net, bpk::backward_layer(s, net->del[l + 1], net->lda[l + 1], wl(net, l), net->ldw[l], rows, net->n[l],
+                                      net->n[l + 1], net->act[l], net->lda[l], net->del[l], net->lda[l]));
+    if (l == 0 && in.act) {
+      BP_HIP(net, bpk::onehot_update(s, in.act, in.n_active, rows, net->del[1], net->lda[1], net->n[0], net->n[1],
+                                     wl(net, 0), vl(net, 0), net->ldw[0], lr, mom));
+      continue;
+    }
+    const float* A = (l == 0) ? in.x : net->act[l];
+    const int ldA = (l == 0) ? net->n[0] : net->lda[l];
+    BP_HIP(net, bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
+                                   wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk));
+    BP_HIP(net, bpk::bias_update(s, net->del[l + 1], net->lda[l + 1], rows, net->n[l + 1], wbias(net, l),
+                                 vbias(net, l), lr, mom));
+  }
+  return BP_OK;
+}
+
+int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr, float mom,
+          double* sse_out) {
+  if (n == 0) {
+    if (sse_out) *sse_out = 0.0;
+    return BP_OK;
+  }
+  const int64_t rows_max = std::min<int64_t>(batch, n);
+  int rc = ensure_workspace(net, rows_max);
+  if (rc) return rc;
+  const int64_t nb = (n + batch - 1) / batch;
+  const size_t per = (size_t)sse_blocks(net, in, (int)rows_max);
+  rc = ensure_sse(net, per * (size_t)nb);
+  if (rc) return rc;
+  size_t used = 0;
+  for (int64_t p0 = 0; p0 < n; p0 += batch) {
+    const int rows = (int)std::min<int64_t>(batch, n - p0);
+    BatchInput b = in;
+    if (b.x) b.x += (size_t)p0 * net->n[0];
+    if (b.act) b.act += (size_t)p0 * b.n_active;
+    rc = run_forward(net, b, rows, targets + (size_t)p0 * net->n[net->L], net->sse_part + used, nullptr, 0,
+                     net->act.data());
+    if (rc) return rc;
+    used += (size_t)sse_blocks(net, b, rows);
+    rc = run_backward_update(net, b, rows, lr, mom);
+    if (rc) return rc;
+  }
+  BP_HIP(net, bpk::sse_reduce(net->stream, net->sse_part, (int)used, net->sse_dev));
+  if (sse_out) {
+    BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, net->stream));
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+  }
+  return BP_OK;
+}
+
+int forward_only(bp_net* net, const BatchInput& in, int64_t n, float* out) {
+  if (n == 0) return BP_OK;
+  const int64_t chunk = std::min<int64_t>(n, 8192);
+  // ping-pong activation buffers sized for the widest hidden layer
+  int widest = 4;
+  for (int l = 1; l < net->L; ++l) widest = std::max(widest, net->lda[l]);
+  const size_t need = (size_t)chunk * widest;
+  if (net->L > 1 && need > net->fwd_cap) {
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+    free_ptr(net->fwd_tmp[0]);
+    free_ptr(net->fwd_tmp[1]);
+    net->fwd_tmp[0] = net->fwd_tmp[1] = nullptr;
+    net->fwd_cap = 0;
+    BP_HIP(net, hipMalloc(&net->fwd_tmp[0], sizeof(float) * need));
+    BP_HIP(net, hipMalloc(&net->fwd_tmp[1], sizeof(float) * need));
+    net->fwd_cap = need;
+  }
+  std::vector<float*> acts(net->L + 1, nullptr);
+  for (int l = 1; l < net->L; ++l) acts[l] = net->fwd_tmp[l & 1];
+  for (int64_t p0 = 0; p0 < n; p0 += chunk) {
+    const int rows = (int)std::min<int64_t>(chunk, n - p0);
+    BatchInput b = in;
+    if (b.x) b.x += (size_t)p0 * net->n[0];
+    if (b.act) b.act += (size_t)p0 * b.n_active;
+    int rc = run_forward(net, b, rows, nullptr, nullptr, out + (size_t)p0 * net->n[net->L], net->n[net->L],
+                         acts.data());
+    if (rc) return rc;
+  }
+  return BP_OK;
+}
+
+int check_net(bp_net* net) { return net ? BP_OK : BP_EINVAL; }
+
+}  // namespace
+
+extern "C" {
+
+int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
+  if (!out) return fail(nullptr, BP_EINVAL, "bp_create: out is NULL");
+  *out = nullptr;
+  if (!layer_sizes) return fail(nullptr, BP_EINVAL, "bp_create: layer_sizes is NULL");
+  if (n_layers < 2) return fail(nullptr, BP_EINVAL, "bp_create: need at least 2 layer sizes");
+  for (int i = 0; i < n_layers; ++i)
+    if (layer_sizes[i] < 1 || layer_sizes[i] > (1 << 24))
+      return fail(nullptr, BP_EINVAL, "bp_create: layer sizes must be in [1, 2^24]");
+  bp_net* net = new bp_net();
+  net->L = n_layers - 1;
+  net->n.assign(layer_sizes, layer_sizes + n_layers);
+  net->ldw.resize(net->L);
+  net->woff.resize(net->L);
+  net->foff.resize(net->L);
+  net->lda.resize(net->L + 1);
+  for (int l = 0; l <= net->L; ++l) net->lda[l] = round4(net->n[l]);
+  for (int l = 0; l < net->L; ++l) {
+    net->ldw[l] = round4(net->n[l + 1]);
+    net->woff[l] = net->wtotal;
+    net->foff[l] = net->nweights;
+    net->wtotal += (int64_t)(net->n[l] + 1) * net->ldw[l];
+    net->nweights += (int64_t)(net->n[l] + 1) * net->n[l + 1];
+  }
+  net->act.assign(net->L + 1, nullptr);
+  net->del.assign(net->L + 1, nullptr);
+  hipError_t e = hipGetDevice(&net->device);
+  if (e == hipSuccess) e = hipMalloc(&net->W, sizeof(float) * net->wtotal);
+  if (e == hipSuccess) e = hipMalloc(&net->V, sizeof(float) * net->wtotal);
+  if (e == hipSuccess) e = hipMemset(net->W, 0, sizeof(float) * net->wtotal);
+  if (e == hipSuccess) e = hipMemset(net->V, 0, sizeof(float) * net->wtotal);
+  if (e != hipSuccess) {
+    hip_fail(nullptr, e, "bp_create");
+    const int code = e == hipErrorOutOfMemory ? BP_ENOMEM : BP_EDEVICE;
+    free_ptr(net->W);
+    free_ptr(net->V);
+    delete net;
+    return code;
+  }
+  *out = net;
+  return BP_OK;
+}
+
+void bp_destroy(bp_net* net) {
+  if (!net) return;
+  (void)hipStreamSynchronize(net->stream);
+  free_workspace(net);
+  free_ptr(net->fwd_tmp[0]);
+  free_ptr(net->fwd_tmp[1]);
+  free_ptr(net->sse_part);
+  free_ptr(net->sse_dev);
+  free_ptr(net->W);
+  free_ptr(net->V);
+  delete net;
+}
+
+int bp_set_stream(bp_net* net, void* hip_stream) {
+  if (check_net(net)) return BP_EINVAL;
+  if (net->stream != (hipStream_t)hip_stream) BP_HIP(net, hipStreamSynchronize(net->stream));
+  net->stream = (hipStream_t)hip_stream;
+  return BP_OK;
+}
+
+int64_t bp_num_weights(const bp_net* net) { return net ? net->nweights : -1; }
+
+int bp_set_weights(bp_net* net, const float* w_host, int64_t n) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!w_host) return fail(net, BP_EINVAL, "bp_set_weights: w_host is NULL");
+  if (n != net->nweights) return fail(net, BP_EINVAL, "bp_set_weights: n != bp_num_weights");
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  BP_HIP(net, hipMemsetAsync(net->W, 0, sizeof(float) * net->wtotal, net->stream));
+  BP_HIP(net, hipMemsetAsync(net->V, 0, sizeof(float) * net->wtotal, net->stream));
+  return copy_layers(net, net->W, w_host, nullptr);
+}
+
+int bp_get_weights(bp_net* net, float* w_host, int64_t n) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!w_host) return fail(net, BP_EINVAL, "bp_get_weights: w_host is NULL");
+  if (n != net->nweights) return fail(net, BP_EINVAL, "bp_get_weights: n != bp_num_weights");
+  return copy_layers(net, net->W, nullptr, w_host);
+}
+
+int bp_set_momentum(bp_net* net, const float* v_host, int64_t n) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!v_host) return fail(net, BP_EINVAL, "bp_set_momentum: v_host is NULL");
+  if (n != net->nweights) return fail(net, BP_EINVAL, "bp_set_momentum: n != bp_num_weights");
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  return copy_layers(net, net->V, v_host, nullptr);
+}
+
+int bp_get_momentum(bp_net* net, float* v_host, int64_t n) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!v_host) return fail(net, BP_EINVAL, "bp_get_momentum: v_host is NULL");
+  if (n != net->nweights) return fail(net, BP_EINVAL, "bp_get_momentum: n != bp_num_weights");
+  return copy_layers(net, net->V, nullptr, v_host);
+}
+
+static int check_train(bp_net* net, const void* in, const float* targets, int64_t n, int32_t batch,
+                       const char* who) {
+  if (check_net(net)) return BP_EINVAL;
+  std::string w(who);
+  if (n < 0) return fail(net, BP_EINVAL, w + ": n_patterns < 0");
+  if (n > ((int64_t)1 << 31) - 1) return fail(net, BP_EINVAL, w + ": n_patterns too large");
+  if (batch < 1) return fail(net, BP_EINVAL, w + ": batch < 1");
+  if (n > 0 && (!in || !targets)) return fail(net, BP_EINVAL, w + ": NULL input or target pointer");
+  if (n > 0 && (!aligned_ptr(in, 4) || !aligned_ptr(targets, 4)))
+    return fail(net, BP_EINVAL, w + ": pointers must be 4-byte aligned");
+  return BP_OK;
+}
+
+int bp_train_batches(bp_net* net, const float* inputs_dev, const float* targets_dev, int64_t n_patterns,
+                     int32_t batch, float lr, float momentum, double* sse_out) {
+  int rc = check_train(net, inputs_dev, targets_dev, n_patterns, batch, "bp_train_batches");
+  if (rc) return rc;
+  BatchInput in;
+  in.x = inputs_dev;
+  return train(net, in, targets_dev, n_patterns, batch, lr, momentum, sse_out);
+}
+
+int bp_train_batches_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, const float* targets_dev,
+                            int64_t n_patterns, int32_t batch, float lr, float momentum, double* sse_out) {
+  int rc = check_train(net, active_dev, targets_dev, n_patterns, batch, "bp_train_batches_onehot");
+  if (rc) return rc;
+  if (n_active < 1 || n_active > net->n[0])
+    return fail(net, BP_EINVAL, "bp_train_batches_onehot: n_active must be in [1, n_0]");
+  BatchInput in;
+  in.act = active_dev;
+  in.n_active = n_active;
+  return train(net, in, targets_dev, n_patterns, batch, lr, momentum, sse_out);
+}
+
+int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* outputs_dev) {
+  if (check_net(net)) return BP_EINVAL;
+  if (n_patterns < 0 || n_patterns > ((int64_t)1 << 31) - 1)
+    return fail(net, BP_EINVAL, "bp_forward: bad n_patterns");
+  if (n_patterns > 0 && (!inputs_dev || !outputs_dev)) return fail(net, BP_EINVAL, "bp_forward: NULL pointer");
+  BatchInput in;
+  in.x = inputs_dev;
+  return forward_only(net, in, n_patterns, outputs_dev);
+}
+
+int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, int64_t n_patterns,
+                      float* outputs_dev) {
+  if (check_net(net)) return BP_EINVAL;
+  if (n_patterns < 0 || n_patterns > ((int64_t)1 << 31) - 1)
+    return fail(net, BP_EINVAL, "bp_forward_onehot: bad n_patterns");
+  if (n_patterns > 0 && (!active_dev || !outputs_dev))
+    return fail(net, BP_EINVAL, "bp_forward_onehot: NULL pointer");
+  if (n_active < 1 || n_active > net->n[0])
+    return fail(net, BP_EINVAL, "bp_forward_onehot: n_active must be in [1, n_0]");
+  BatchInput in;
+  in.act = active_dev;
+  in.n_active = n_active;
+  return forward_only(net, in, n_patterns, outputs_dev);
+}
+
+const char* bp_last_error(const bp_net* net) { return net ? net->err.c_str() : g_create_err.c_str(); }
+
+}  // extern "C"

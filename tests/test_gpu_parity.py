@@ -1,0 +1,265 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle.
+
+Every case runs the same seeded inputs through libbp.so and through the
+oracle (double storage, the plain definition) and compares:
+  * weights and momentum after one pooled update: per layer
+    max |w_gpu - w_ref| / max |w_ref| <= 1e-5;
+  * summed squared error of every epoch: relative difference <= 1e-3;
+  * forward outputs: absolute difference <= 1e-5 (outputs lie in [0, 1]).
+Shapes span several 128 x 128 tiles with ragged tails, the named workloads
+run at their full layer sizes and batch, and the edge cases of the method
+(empty input, short last batch, batch 1, single-layer nets, lr = 0) are
+covered.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1801_01554_amd import bp
+from paper_1801_01554_amd import workloads as wl
+from parity_util import SSE_TOL, W_TOL, layer_views, load_golden, rel, rel_maxabs, to_device
+
+pytestmark = pytest.mark.gpu
+FWD_TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU parity tests need a ROCm device"
+    bp.lib()
+    return torch.device("cuda:0")
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _oracle_net(w):
+    o = oracle.OracleNet(w.sizes, 64)
+    o.set_weights(w.weights.astype(np.float64))
+    return o
+
+
+def _oracle_epoch(o, w, batch, lr, mom, n=None):
+    n = w.n_patterns if n is None else n
+    kw = {"active": w.active[:n]} if w.active is not None else {"x": w.inputs[:n]}
+    return o.train_epoch(w.targets[:n], batch, lr, mom, **kw)
+
+
+def _gpu_epoch(net, w, x, a, t, batch, lr, mom, n=None):
+    n = w.n_patterns if n is None else n
+    if a is not None:
+        return net.train_batches(t[:n], batch, lr, mom, active=a[:n])
+    return net.train_batches(t[:n], batch, lr, mom, inputs=x[:n])
+
+
+def _check_update(w, dev, batch, lr, mom, n=None, what=""):
+    n = w.n_patterns if n is None else n
+    _say(f"case {what}: sizes={w.sizes} n={n} batch={batch} onehot={w.active is not None}")
+    x, a, t = to_device(w, dev)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    sse_g = _gpu_epoch(net, w, x, a, t, batch, lr, mom, n)
+    wg, vg = net.get_weights(), net.get_momentum()
+    o = _oracle_net(w)
+    sse_o = _oracle_epoch(o, w, batch, lr, mom, n)
+    ew = rel_maxabs(w.sizes, wg, o.get_weights())
+    ev = rel_maxabs(w.sizes, vg, o.get_momentum())
+    _say(f"  weights rel err per layer {ew}, momentum {ev}, sse gpu {sse_g} oracle {sse_o}")
+    assert max(ew) <= W_TOL, ew
+    if n > 0:
+        assert rel(sse_g, sse_o) <= SSE_TOL
+    net.close()
+    return ew, ev, sse_g, sse_o
+
+
+# --------------------------------------------------------------------------- forward
+@pytest.mark.parametrize("sizes,n", [((203, 80, 26), 1000), ((130, 257, 67), 300), ((1, 1), 5), ((64, 1), 129),
+                                     ((1024, 4096, 1024), 512), ((512, 2048, 2048, 2048, 64), 256),
+                                     ((33, 5, 7, 9, 2), 40)])
+def test_forward_matches_oracle(dev, sizes, n):
+    w = wl.make_custom(sizes, n, seed=sum(sizes) + n, input_kind="normal")
+    _say(f"case forward sizes={sizes} n={n}")
+    net = bp.Net(sizes)
+    net.set_weights(w.weights)
+    y = net.forward(inputs=torch.from_numpy(w.inputs).to(dev)).cpu().numpy()
+    ref = _oracle_net(w).forward(x=w.inputs)
+    err = np.max(np.abs(y - ref)) if n else 0.0
+    _say(f"  max abs err {err}")
+    assert err <= FWD_TOL
+
+
+@pytest.mark.parametrize("sizes,n", [((203, 120, 26), 700), ((203, 300, 26), 65), ((50, 9), 17)])
+def test_onehot_forward_matches_oracle(dev, sizes, n):
+    w = wl.make_custom(sizes, n, seed=7 + n, onehot=True, init="uniform0.3")
+    _say(f"case forward onehot sizes={sizes} n={n}")
+    net = bp.Net(sizes)
+    net.set_weights(w.weights)
+    y = net.forward(active=torch.from_numpy(w.active).to(dev)).cpu().numpy()
+    ref = _oracle_net(w).forward(active=w.active)
+    assert np.max(np.abs(y - ref)) <= FWD_TOL
+
+
+# --------------------------------------------------------------------------- one update, full sizes
+@pytest.mark.parametrize("name", wl.ORDER)
+def test_first_update_full_size(dev, name):
+    w = wl.make(name, n_patterns=wl.SPECS[name].batch)
+    _check_update(w, dev, w.batch, w.lr, w.momentum, what=f"first update {name}")
+
+
+# --------------------------------------------------------------------------- ragged shapes
+@pytest.mark.parametrize("sizes,n,batch,onehot", [
+    ((37, 70, 130, 5), 77, 77, False),
+    ((300, 129, 1), 257, 257, False),
+    ((129, 65, 33), 3, 1, False),
+    ((5, 3), 10, 4, False),
+    ((203, 120, 26), 32, 32, True),
+    ((203, 300, 26), 600, 300, True),
+    ((20, 4), 9, 9, True),
+    ((1030, 260, 70), 1100, 1100, False),
+])
+def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
+    w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
+                       init="uniform0.3" if onehot else "fanin")
+    _check_update(w, dev, batch, 0.05, 0.9, what="ragged")
+
+
+# --------------------------------------------------------------------------- epochs
+@pytest.mark.parametrize("name", ["nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16"])
+def test_epoch_errors_nettalk(dev, name):
+    w = wl.make(name)
+    s = w.spec
+    _say(f"case epochs {name}: {s.epochs} epochs of {s.n_patterns} patterns, batch {s.batch}")
+    x, a, t = to_device(w, dev)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    o = _oracle_net(w)
+    for e in range(s.epochs):
+        sg = _gpu_epoch(net, w, x, a, t, s.batch, w.lr, w.momentum)
+        so = _oracle_epoch(o, w, s.batch, w.lr, w.momentum)
+        _say(f"  epoch {e}: sse gpu {sg:.9g} oracle {so:.9g} rel {rel(sg, so):.3g}")
+        assert rel(sg, so) <= SSE_TOL
+    _say(f"  final weights rel err {rel_maxabs(w.sizes, net.get_weights(), o.get_weights())}")
+
+
+@pytest.mark.parametrize("name", ["wide-1024-4096-1024", "deep-512-2048x3-64"])
+def test_epoch_errors_dense_against_stored(dev, name):
+    g = load_golden(name)
+    if g is None:
+        pytest.skip(f"no stored oracle epoch errors for {name}")
+    w = wl.make(name)
+    s = w.spec
+    _say(f"case epoch {name} against stored oracle errors")
+    x, a, t = to_device(w, dev)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    ref = g["storage64"]["epoch_sse"]
+    for e in range(s.epochs):
+        sg = _gpu_epoch(net, w, x, a, t, s.batch, w.lr, w.momentum)
+        _say(f"  epoch {e}: sse gpu {sg:.9g} oracle {ref[e]:.9g} rel {rel(sg, ref[e]):.3g}")
+        assert rel(sg, ref[e]) <= SSE_TOL
+
+
+# --------------------------------------------------------------------------- properties
+def test_onehot_path_equals_dense_path(dev):
+    w = wl.make("nettalk-80-b1024")
+    _say("case onehot vs dense nettalk-80-b1024")
+    x = torch.from_numpy(w.dense_inputs()).to(dev)
+    a = torch.from_numpy(w.active).to(dev)
+    t = torch.from_numpy(w.targets).to(dev)
+    n1, n2 = bp.Net(w.sizes), bp.Net(w.sizes)
+    n1.set_weights(w.weights)
+    n2.set_weights(w.weights)
+    s1 = n1.train_batches(t, w.batch, w.lr, w.momentum, active=a)
+    s2 = n2.train_batches(t, w.batch, w.lr, w.momentum, inputs=x)
+    assert rel(s1, s2) <= 1e-5
+    assert max(rel_maxabs(w.sizes, n1.get_weights(), n2.get_weights())) <= W_TOL
+
+
+@pytest.mark.parametrize("name,n", [("nettalk-120-b512", 2048), ("deep-512-2048x3-64", 8192)])
+def test_run_to_run_identical(dev, name, n):
+    w = wl.make(name, n_patterns=n)
+    _say(f"case determinism {name} n={n}")
+    x, a, t = to_device(w, dev)
+    res = []
+    for _ in range(2):
+        net = bp.Net(w.sizes)
+        net.set_weights(w.weights)
+        s = _gpu_epoch(net, w, x, a, t, w.batch, w.lr, w.momentum, n)
+        res.append((s, net.get_weights(), net.get_momentum()))
+        net.close()
+    assert res[0][0] == res[1][0]
+    np.testing.assert_array_equal(res[0][1], res[1][1])
+    np.testing.assert_array_equal(res[0][2], res[1][2])
+
+
+def test_split_calls_equal_one_call(dev):
+    # One call over 3 batches == three calls of one batch each (momentum carried).
+    w = wl.make_custom((40, 30, 6), 96, seed=5)
+    x, a, t = to_device(w, dev)
+    n1, n2 = bp.Net(w.sizes), bp.Net(w.sizes)
+    n1.set_weights(w.weights)
+    n2.set_weights(w.weights)
+    s1 = n1.train_batches(t, 32, 0.1, 0.9, inputs=x)
+    s2 = sum(n2.train_batches(t[i:i + 32], 32, 0.1, 0.9, inputs=x[i:i + 32]) for i in (0, 32, 64))
+    np.testing.assert_array_equal(n1.get_weights(), n2.get_weights())
+    assert rel(s1, s2) <= 1e-12
+
+
+def test_exact_resume_through_momentum(dev):
+    w = wl.make_custom((30, 20, 4), 64, seed=6)
+    x, a, t = to_device(w, dev)
+    full = bp.Net(w.sizes)
+    full.set_weights(w.weights)
+    full.train_batches(t, 16, 0.1, 0.9, inputs=x)
+    full.train_batches(t, 16, 0.1, 0.9, inputs=x)
+    part = bp.Net(w.sizes)
+    part.set_weights(w.weights)
+    part.train_batches(t, 16, 0.1, 0.9, inputs=x)
+    wts, mom = part.get_weights(), part.get_momentum()
+    resumed = bp.Net(w.sizes)
+    resumed.set_weights(wts)
+    resumed.set_momentum(mom)
+    resumed.train_batches(t, 16, 0.1, 0.9, inputs=x)
+    np.testing.assert_array_equal(resumed.get_weights(), full.get_weights())
+
+
+def test_lr_zero_and_empty_input(dev):
+    w = wl.make_custom((30, 20, 4), 50, seed=8)
+    x, a, t = to_device(w, dev)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    s = net.train_batches(t, 7, 0.0, 0.9, inputs=x)
+    np.testing.assert_array_equal(net.get_weights(), w.weights)
+    ref = np.sum((w.targets.astype(np.float64) - _oracle_net(w).forward(x=w.inputs)) ** 2)
+    assert rel(s, ref) <= 1e-5
+    assert net.train_batches(t[:0], 7, 0.1, 0.9, inputs=x[:0]) == 0.0
+    np.testing.assert_array_equal(net.get_weights(), w.weights)
+
+
+def test_bad_arguments_leave_net_unchanged(dev):
+    w = wl.make_custom((30, 20, 4), 10, seed=9, onehot=True)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    t = torch.from_numpy(w.targets).to(dev)
+    a = torch.from_numpy(w.active).to(dev)
+    h, sse = net._h, ctypes.c_double(-1.0)
+    assert bp.bp_train_batches_onehot(h, a.data_ptr(), 7, t.data_ptr(), 10, 0, 0.1, 0.9, sse) == bp.BP_EINVAL
+    assert bp.bp_train_batches_onehot(h, a.data_ptr(), 0, t.data_ptr(), 10, 4, 0.1, 0.9, sse) == bp.BP_EINVAL
+    assert bp.bp_train_batches_onehot(h, a.data_ptr(), 31, t.data_ptr(), 10, 4, 0.1, 0.9, sse) == bp.BP_EINVAL
+    assert bp.bp_train_batches_onehot(h, a.data_ptr(), 7, t.data_ptr(), -1, 4, 0.1, 0.9, sse) == bp.BP_EINVAL
+    assert bp.bp_train_batches(h, 0, t.data_ptr(), 10, 4, 0.1, 0.9, sse) == bp.BP_EINVAL
+    assert bp.bp_set_weights(h, np.zeros(5, np.float32)) == bp.BP_EINVAL
+    assert "n != bp_num_weights" in bp.bp_last_error(h)
+    np.testing.assert_array_equal(net.get_weights(), w.weights)
+    assert np.all(net.get_momentum() == 0)
+
+
+@pytest.mark.parametrize("sizes,onehot", [((12, 5), False), ((40, 3), True), ((7, 1, 1), False), ((9, 2), True)])
+def test_single_and_degenerate_layers(dev, sizes, onehot):
+    w = wl.make_custom(sizes, 23, seed=len(sizes) + sizes[0], onehot=onehot,
+                       init="uniform0.3" if onehot else "fanin")
+    _check_update(w, dev, 10, 0.2, 0.9, what="degenerate")
