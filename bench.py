@@ -1,0 +1,321 @@
+"""Throughput of pooled back-propagation on one MI355X, in connections per second.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pooled update: forward pass, output and hidden deltas, summed
+change and learning-rate/momentum update over one batch (all on the GPU,
+inputs resident in HBM).  The primary workload is the NETtalk-shaped
+203-120-26 net with one-hot 7 x 29 window inputs, batch 512, 20,000
+patterns; its steps follow the epoch structure (40 updates per epoch, the
+last of 32 patterns).  The wide (1024-4096-1024, batch 4096) and deep
+(512-2048-2048-2048-64, batch 8192) dense nets run one full epoch each and
+are reported under "secondary".
+
+value = connections x patterns presented / wall time (the paper's
+definition, section 7.1: bias connections included, update frequency and
+cheaper input connections not accounted for).
+
+Per-kernel device times come from a second pass over the same steps in which
+the library brackets every launch with HIP events on its stream; the
+dominant kernel's algorithmic work per launch divided by its average
+duration gives the roofline entry.  The oracle (CPU, test infrastructure) is
+timed on a bounded sample for the CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "connection-updates/sec (fwd+bwd+update) and % fp32 MFMA peak, 1 MI355X"
+PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix peak, flop/s
+PEAK_HBM = 8.0e12           # MI355X HBM3E, bytes/s
+PAPER_GF11_CPS = 9.01e8     # section 6.3, Table 1: 356 processors, tree summation
+PRIMARY = "nettalk-120-b512"
+SECONDARY = ("wide-1024-4096-1024", "deep-512-2048x3-64")
+GEMM_KINDS = ("forward", "output", "backward", "change")
+KERNEL_NAMES = {
+    "forward": "gemm_kernel<..., EpiSigmoid>",
+    "output": "gemm_kernel<..., EpiOutputDelta>",
+    "backward": "gemm_kernel<..., EpiHiddenDelta>",
+    "change": "gemm_kernel<..., EpiUpdate|EpiPartial>",
+    "splitk": "splitk_update_kernel",
+    "bias": "bias_update_kernel",
+    "gather": "onehot_forward_kernel",
+    "scatter": "onehot_update_kernel",
+    "reduce": "sse_reduce_kernel",
+}
+
+
+def kind_work(sizes, rows, onehot, n_active, splits_of):
+    """Algorithmic (flops, HBM bytes) of each kernel kind for one update over `rows` patterns."""
+    w = {}
+
+    def add(kind, f, b):
+        f0, b0 = w.get(kind, (0.0, 0.0))
+        w[kind] = (f0 + f, b0 + b)
+
+    L = len(sizes) - 1
+    R = float(rows)
+    for l in range(L):
+        ni, no = sizes[l], sizes[l + 1]
+        if l == 0 and onehot:
+            add("gather", R * no * (n_active + 1), 4 * (R * n_active + (ni + 1) * no + R * no))
+            add("scatter", R * no * (n_active + 1), 4 * (R * n_active + R * no) + 16 * (ni + 1) * no)
+        else:
+            if l == L - 1:
+                add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + 2 * R * no))
+            else:
+                add("forward", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + R * no))
+            upd = 16.0 * ni * no
+            if splits_of(ni, no, rows) > 1:
+                add("change", 2 * R * ni * no, 4 * (R * ni + R * no))
+                add("splitk", 0.0, upd)
+            else:
+                add("change", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
+            add("bias", R * no, 4 * R * no + 16 * no)
+        if l >= 1:
+            add("backward", 2 * R * no * ni, 4 * (R * no + ni * no + 2 * R * ni))
+    return w
+
+
+def choose_splits(M, N, K):
+    """Mirror of the library's split-K choice (128 x 128 tiles), for work accounting only."""
+    tiles = -(-M // 128) * -(-N // 128)
+    if K < 1024 or tiles >= 128:
+        return 1
+    s = -(-256 // tiles)
+    return max(1, min(s, K // 256))
+
+
+def schedule(spec, steps):
+    """(first pattern, patterns, updates) calls covering `steps` updates in epoch order."""
+    per_epoch = -(-spec.n_patterns // spec.batch)
+    calls = []
+    full, rem = divmod(steps, per_epoch)
+    calls += [(0, spec.n_patterns, per_epoch)] * full
+    if rem:
+        calls.append((0, rem * spec.batch, rem))
+    return calls
+
+
+def step_rows(spec, calls):
+    rows = []
+    for p0, n, _ in calls:
+        for b0 in range(p0, p0 + n, spec.batch):
+            rows.append(min(spec.batch, p0 + n - b0))
+    return rows
+
+
+def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
+    spec = wl.SPECS[name]
+    t0 = time.time()
+    w = wl.make(name)
+    log(f"[{name}] generated {w.n_patterns} patterns in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    t = torch.from_numpy(w.targets).to(dev)
+    x = torch.from_numpy(w.inputs).to(dev) if w.inputs is not None else None
+    a = torch.from_numpy(w.active).to(dev) if w.active is not None else None
+    net = bp.Net(w.sizes)
+
+    def run(calls):
+        for p0, n, _ in calls:
+            if a is not None:
+                net.train_batches(t[p0:p0 + n], spec.batch, w.lr, w.momentum, active=a[p0:p0 + n], want_sse=False)
+            else:
+                net.train_batches(t[p0:p0 + n], spec.batch, w.lr, w.momentum, inputs=x[p0:p0 + n], want_sse=False)
+
+    calls = schedule(spec, steps)
+    patterns = sum(n for _, n, _ in calls)
+    if warmup:
+        net.set_weights(w.weights)
+        run(schedule(spec, warmup))
+    net.set_weights(w.weights)            # timed run starts from the workload's initial state
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    ev0.record()
+    run(calls)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    secs = ev0.elapsed_time(ev1) / 1e3
+    log(f"[{name}] {steps} steps, {patterns} patterns in {secs * 1e3:.2f} ms (wall {wall * 1e3:.2f} ms)")
+
+    # profile pass: the same steps with every launch bracketed by events
+    net.set_weights(w.weights)
+    net.profile(True)
+    run(calls)
+    rep = net.profile_report()
+    net.profile(False)
+    net.close()
+
+    W = metrics.num_weights(w.sizes)
+    cps = W * patterns / secs
+    flops_step = sum(metrics.dense_flops_per_pattern(w.sizes, r) * r for r in step_rows(spec, calls))
+    work = {}
+    for r in step_rows(spec, calls):
+        for k, (f, b) in kind_work(w.sizes, r, w.active is not None, 7, choose_splits).items():
+            f0, b0 = work.get(k, (0.0, 0.0))
+            work[k] = (f0 + f, b0 + b)
+    kernels = {}
+    for k, (cnt, ms) in rep.items():
+        if cnt == 0:
+            continue
+        f, b = work.get(k, (0.0, 0.0))
+        s = ms / 1e3
+        kernels[k] = {"name": KERNEL_NAMES[k], "launches": cnt, "avg_us": ms * 1e3 / cnt, "total_ms": ms,
+                      "tflops": f / s / 1e12 if s > 0 else None, "gbps": b / s / 1e9 if s > 0 else None,
+                      "flops_per_launch": f / cnt, "bytes_per_launch": b / cnt}
+    dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+    dk = kernels[dom]
+    f, b = work.get(dom, (0.0, 0.0))
+    mfma_bound = f / PEAK_FP32_MFMA >= b / PEAK_HBM
+    if mfma_bound:
+        ach, peak, unit = dk["tflops"], PEAK_FP32_MFMA / 1e12, "TFLOP/s"
+    else:
+        ach, peak, unit = dk["gbps"], PEAK_HBM / 1e9, "GB/s"
+    roof = {"bound": "mfma" if mfma_bound else "hbm", "kernel": dk["name"], "kind": dom,
+            "achieved": ach, "peak": peak, "unit": unit, "frac": ach / peak,
+            "avg_launch_us": dk["avg_us"], "work_per_launch": dk["flops_per_launch"] if mfma_bound else dk["bytes_per_launch"],
+            "traffic": traffic_for(name, dom)}
+    gemm_ms = sum(kernels[k]["total_ms"] for k in GEMM_KINDS if k in kernels)
+    gemm_f = sum(work.get(k, (0, 0))[0] for k in GEMM_KINDS)
+    res = {
+        "workload": name, "net": "-".join(map(str, w.sizes)), "batch": spec.batch, "patterns": patterns,
+        "steps": steps, "warmup": warmup, "seconds": secs, "ms_per_step": secs * 1e3 / steps, "value": cps,
+        "mfma_peak_frac": flops_step / secs / PEAK_FP32_MFMA,
+        "gemm_mfma_frac": (gemm_f / (gemm_ms / 1e3) / PEAK_FP32_MFMA) if gemm_ms > 0 else None,
+        "us_per_update": secs * 1e6 / steps, "roofline": roof, "kernels": kernels,
+        "kernel_time_ms": sum(v["total_ms"] for v in kernels.values()),
+    }
+    return res, w
+
+
+def traffic_for(workload, kind):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it matches the current kernels."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        with open(p) as f:
+            d = json.load(f)
+        src = os.path.join(ROOT, "paper_1801_01554_amd", "csrc", "bp_kernels.hip")
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if d.get("kernel_source_sha256") != sha:
+            return None
+        return d.get("workloads", {}).get(workload, {}).get(kind)
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(w, budget_s, log):
+    """The oracle (double storage) on the host cores, whole epochs of the workload until the budget is spent."""
+    import oracle
+    from paper_1801_01554_amd import metrics
+    spec = w.spec
+    o = oracle.OracleNet(w.sizes, 64)
+    o.set_weights(w.weights.astype("float64"))
+    kw = {"active": w.active} if w.active is not None else {"x": w.inputs}
+    t0 = time.perf_counter()
+    epochs = 0
+    while epochs < spec.epochs:
+        o.train_epoch(w.targets, spec.batch, w.lr, w.momentum, **kw)
+        epochs += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    secs = time.perf_counter() - t0
+    pats = epochs * w.n_patterns
+    v = metrics.num_weights(w.sizes) * pats / secs
+    log(f"[cpu] oracle {epochs} epoch(s), {pats} patterns in {secs:.2f}s on {oracle.get_threads()} threads")
+    return {"value": v, "unit": "connections/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "sample": f"{epochs} of {spec.epochs} epochs of {w.spec.name} ({pats} patterns), {secs:.2f} s"}
+
+
+def cpu_sample_batch(w, log):
+    """The oracle on the first batch only (one pooled update), for the large dense nets."""
+    import oracle
+    from paper_1801_01554_amd import metrics
+    spec = w.spec
+    o = oracle.OracleNet(w.sizes, 64)
+    o.set_weights(w.weights.astype("float64"))
+    n = spec.batch
+    t0 = time.perf_counter()
+    o.train_epoch(w.targets[:n], spec.batch, w.lr, w.momentum, x=w.inputs[:n])
+    secs = time.perf_counter() - t0
+    log(f"[cpu] oracle 1 update of {w.spec.name} in {secs:.2f}s")
+    return {"value": metrics.num_weights(w.sizes) * n / secs, "unit": "connections/s",
+            "cores": oracle.get_threads(), "kind": "oracle", "sample": f"first update ({n} patterns), {secs:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="pooled updates timed (default: the whole workload)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed updates first (default: one epoch)")
+    ap.add_argument("--workload", default=PRIMARY)
+    ap.add_argument("--no-secondary", action="store_true", help="skip the wide and deep dense nets")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for the baseline")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the design notes describe how the "
+              "pooled update would shard across GPUs). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    def log(msg):
+        print(msg, file=sys.stderr, flush=True)
+
+    import torch
+    from paper_1801_01554_amd import bp, metrics
+    from paper_1801_01554_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm device"
+    bp.lib()
+    spec = wl.SPECS[args.workload]
+    per_epoch = -(-spec.n_patterns // spec.batch)
+    steps = args.steps if args.steps is not None else per_epoch * spec.epochs
+    warmup = args.warmup if args.warmup is not None else per_epoch
+    prim, w = run_workload(args.workload, steps, warmup, torch, bp, wl, metrics, log)
+
+    secondary = []
+    if not args.no_secondary:
+        for name in SECONDARY:
+            if name == args.workload:
+                continue
+            s2 = wl.SPECS[name]
+            pe = -(-s2.n_patterns // s2.batch)
+            r, w2 = run_workload(name, pe * s2.epochs, 4, torch, bp, wl, metrics, log)
+            if not args.no_cpu:
+                r["cpu_baseline"] = cpu_sample_batch(w2, log)
+            secondary.append(r)
+            del w2
+            torch.cuda.empty_cache()
+
+    line = {
+        "metric": METRIC, "value": prim["value"], "unit": "connections/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": prim["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "net": prim["net"], "batch": spec.batch,
+                   "patterns_per_epoch": spec.n_patterns, "patterns_timed": prim["patterns"],
+                   "inputs": "one-hot 7x29 window" if spec.onehot else spec.input_kind,
+                   "lr": spec.lr, "momentum": spec.momentum, "parallelism": "single GPU"},
+        "mfma_peak_frac": prim["mfma_peak_frac"], "us_per_update": prim["us_per_update"],
+        "roofline": prim["roofline"], "kernels": prim["kernels"],
+        "context": {"paper_gf11_cps": PAPER_GF11_CPS, "note": "GF11, 356 processors, NETtalk 203-60-26 (section 6.3)"},
+        "secondary": secondary,
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, log)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -122,6 +122,30 @@ int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* 
 int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, int64_t n_patterns,
                       float* outputs_dev);
 
+/* Measurement support (not part of the method).  Kernel kinds a net launches: */
+enum {
+  BP_K_FORWARD = 0,   /* hidden-layer forward product + sigmoid            */
+  BP_K_OUTPUT = 1,    /* output-layer forward product + deltas + error      */
+  BP_K_BACKWARD = 2,  /* hidden-delta product + derivative                  */
+  BP_K_CHANGE = 3,    /* summed-change product (+ momentum update)          */
+  BP_K_SPLITK = 4,    /* ordered split-K reduction + momentum update        */
+  BP_K_BIAS = 5,      /* bias-row column sums + momentum update             */
+  BP_K_GATHER = 6,    /* one-hot first-layer forward                        */
+  BP_K_SCATTER = 7,   /* one-hot first-layer change + momentum update       */
+  BP_K_REDUCE = 8,    /* epoch error reduction                              */
+  BP_K_COUNT = 9
+};
+
+/* on != 0: from now on every kernel launch of this net is bracketed by HIP
+ * events on the net's stream (adds launch overhead; for measurement runs
+ * only); clears the counters.  on == 0: stops recording. */
+int bp_profile(bp_net* net, int on);
+
+/* Waits for the stream and writes, for each kind k < n_kinds (<= BP_K_COUNT),
+ * the number of launches recorded and their summed device time in
+ * milliseconds (launches[k], ms[k]; host arrays). */
+int bp_profile_report(bp_net* net, int64_t* launches, double* ms, int32_t n_kinds);
+
 /* Message describing the last non-OK return on this net (or of bp_create
  * when net is NULL).  Valid until the next call on the net. */
 const char* bp_last_error(const bp_net* net);

@@ -24,7 +24,8 @@ LIB_PATH = os.path.join(HERE, "libbp.so")
 BP_OK, BP_EINVAL, BP_ENOMEM, BP_EDEVICE = 0, -1, -2, -3
 EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set_weights", "bp_get_weights",
            "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
-           "bp_forward_onehot", "bp_last_error")
+           "bp_forward_onehot", "bp_profile", "bp_profile_report", "bp_last_error")
+KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce")
 
 _lib = None
 _vp = ctypes.c_void_p
@@ -62,6 +63,8 @@ def lib():
                                                    ctypes.c_float, ctypes.c_float, _f64p]),
         "bp_forward": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, _vp]),
         "bp_forward_onehot": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int64, _vp]),
+        "bp_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
+        "bp_profile_report": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64), _f64p, ctypes.c_int32]),
         "bp_last_error": (ctypes.c_char_p, [_vp]),
     }
     for name, (res, args) in sig.items():
@@ -127,6 +130,19 @@ def bp_forward(h, inputs_ptr: int, n: int, outputs_ptr: int) -> int:
 
 def bp_forward_onehot(h, active_ptr: int, n_active: int, n: int, outputs_ptr: int) -> int:
     return lib().bp_forward_onehot(h, _vp(active_ptr), n_active, n, _vp(outputs_ptr))
+
+
+def bp_profile(h, on: bool) -> int:
+    return lib().bp_profile(h, 1 if on else 0)
+
+
+def bp_profile_report(h):
+    """Returns (rc, {kind: (launches, ms)})."""
+    n = len(KINDS)
+    cnt = (ctypes.c_int64 * n)()
+    ms = (ctypes.c_double * n)()
+    rc = lib().bp_profile_report(h, cnt, ms, n)
+    return rc, {k: (int(cnt[i]), float(ms[i])) for i, k in enumerate(KINDS)}
 
 
 def bp_last_error(h) -> str:
@@ -206,6 +222,14 @@ class Net:
             rc = bp_train_batches(self._h, xp, tp, n, int(batch), float(lr), float(momentum), sse)
         self._chk(rc)
         return sse.value if want_sse else None
+
+    def profile(self, on: bool) -> None:
+        self._chk(bp_profile(self._h, on))
+
+    def profile_report(self) -> dict:
+        rc, rep = bp_profile_report(self._h)
+        self._chk(rc)
+        return rep
 
     def forward(self, inputs=None, active=None) -> "torch.Tensor":
         src = active if active is not None else inputs

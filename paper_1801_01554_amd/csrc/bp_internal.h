@@ -31,14 +31,23 @@ hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const fl
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N,
                           int K, const float* act, int lda, float* out, int ldo);
 
+// Number of K-splits change_update uses for an M x N change summed over K
+// rows (1 = the product applies the update itself).
+int change_splits(int M, int N, int K);
+
 // Floats of split workspace change_update needs for an M x N change summed over K rows.
 size_t change_update_workspace(int M, int N, int K);
 
 // Weight change and update for the non-bias rows:
 //   G[m][n] = sum_k A[k][m] D[k][n];  V = lr G + mom V;  W += V   (m < M, n < N).
-// `ws` must hold change_update_workspace(M, N, K) floats (may be NULL if 0).
+// With change_splits(M, N, K) > 1 this launch only writes the partial sums
+// to `ws` (change_update_workspace floats) and splitk_finish must follow.
 hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N,
                          int K, float* W, float* V, int ldw, float lr, float mom, float* ws);
+
+// Sums the split partials of change_update in split order, then updates V and W.
+hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
+                         const float* ws);
 
 // Bias-row change and update: G[n] = sum_{k < rows} D[k][n];  V = lr G + mom V;  W += V.
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb,

@@ -506,6 +506,8 @@ hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W
   return launch_gemm<kBM, kBN, false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 
+int change_splits(int M, int N, int K) { return choose_splits(M, N, K); }
+
 size_t change_update_workspace(int M, int N, int K) {
   const int sp = choose_splits(M, N, K);
   if (sp <= 1) return 0;
@@ -522,13 +524,18 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
     return launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
-  const size_t stride = (size_t)M * ldp;
-  EpiPartial e{ws, ldp, stride};
-  hipError_t err = launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
-  if (err != hipSuccess) return err;
+  EpiPartial e{ws, ldp, (size_t)M * ldp};
+  return launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
+}
+
+hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
+                         const float* ws) {
+  const int sp = choose_splits(M, N, K);
+  if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
+  const int ldp = (N + 3) / 4 * 4;
   const size_t total = (size_t)M * N;
-  splitk_update_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(ws, sp, stride, M, N, ldp,
-                                                                                         W, V, ldw, lr, mom);
+  splitk_update_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
+      ws, sp, (size_t)M * ldp, M, N, ldp, W, V, ldw, lr, mom);
   return hipGetLastError();
 }
 

@@ -43,6 +43,16 @@ struct bp_net {
   double* sse_part = nullptr;
   size_t sse_cap = 0;
   double* sse_dev = nullptr;
+  // measurement: launches bracketed by events while `prof` is set
+  bool prof = false;
+  struct Rec {
+    int kind;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> ev_pool;
+  int64_t prof_n[BP_K_COUNT] = {};
+  double prof_ms[BP_K_COUNT] = {};
   std::string err;
 };
 
@@ -69,6 +79,32 @@ int hip_fail(bp_net* net, hipError_t e, const char* what) {
   } while (0)
 
 int round4(int v) { return (v + 3) / 4 * 4; }
+
+hipEvent_t take_event(bp_net* net) {
+  if (!net->ev_pool.empty()) {
+    hipEvent_t e = net->ev_pool.back();
+    net->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Runs one launch; while profiling, brackets it with events on the stream.
+template <class F>
+hipError_t launch(bp_net* net, int kind, F&& f) {
+  if (!net->prof) return f();
+  hipEvent_t a = take_event(net), b = take_event(net);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, net->stream);
+  if (e == hipSuccess) e = f();
+  if (e == hipSuccess) e = hipEventRecord(b, net->stream);
+  net->recs.push_back({kind, a, b});
+  return e;
+}
+
+#define BP_LAUNCH(net, kind, expr) BP_HIP(net, launch(net, kind, [&]() { return (expr); }))
 
 void free_ptr(void* p) {
   if (p) (void)hipFree(p);
@@ -156,18 +192,21 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
     float* dst = last ? (T ? net->del[L] : out) : acts[l + 1];
     const int ldd = last ? (T ? net->lda[L] : ldo) : net->lda[l + 1];
     if (l == 0 && in.act) {
-      BP_HIP(net, bpk::onehot_forward(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], net->n[0], net->n[1],
-                                      (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part));
+      BP_LAUNCH(net, BP_K_GATHER,
+                bpk::onehot_forward(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], net->n[0], net->n[1],
+                                    (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part));
       continue;
     }
     const float* A = (l == 0) ? in.x : acts[l];
     const int ldA = (l == 0) ? net->n[0] : net->lda[l];
     if (last && T)
-      BP_HIP(net, bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
-                                            wbias(net, l), T, net->n[L], dst, ldd, sse_part));
+      BP_LAUNCH(net, BP_K_OUTPUT,
+                bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
+                                          wbias(net, l), T, net->n[L], dst, ldd, sse_part));
     else
-      BP_HIP(net, bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
-                                     wbias(net, l), dst, ldd));
+      BP_LAUNCH(net, BP_K_FORWARD,
+                bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
+                                   wbias(net, l), dst, ldd));
   }
   return BP_OK;
 }
@@ -184,19 +223,27 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
   for (int l = net->L - 1; l >= 0; --l) {
     // Hidden deltas of layer l use W_l before its update.
     if (l >= 1)
-      BP_HIP(net, bpk::backward_layer(s, net->del[l + 1], net->lda[l + 1], wl(net, l), net->ldw[l], rows, net->n[l],
-                                      net->n[l + 1], net->act[l], net->lda[l], net->del[l], net->lda[l]));
+      BP_LAUNCH(net, BP_K_BACKWARD,
+                bpk::backward_layer(s, net->del[l + 1], net->lda[l + 1], wl(net, l), net->ldw[l], rows, net->n[l],
+                                    net->n[l + 1], net->act[l], net->lda[l], net->del[l], net->lda[l]));
     if (l == 0 && in.act) {
-      BP_HIP(net, bpk::onehot_update(s, in.act, in.n_active, rows, net->del[1], net->lda[1], net->n[0], net->n[1],
-                                     wl(net, 0), vl(net, 0), net->ldw[0], lr, mom));
+      BP_LAUNCH(net, BP_K_SCATTER,
+                bpk::onehot_update(s, in.act, in.n_active, rows, net->del[1], net->lda[1], net->n[0], net->n[1],
+                                   wl(net, 0), vl(net, 0), net->ldw[0], lr, mom));
       continue;
     }
     const float* A = (l == 0) ? in.x : net->act[l];
     const int ldA = (l == 0) ? net->n[0] : net->lda[l];
-    BP_HIP(net, bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
-                                   wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk));
-    BP_HIP(net, bpk::bias_update(s, net->del[l + 1], net->lda[l + 1], rows, net->n[l + 1], wbias(net, l),
-                                 vbias(net, l), lr, mom));
+    BP_LAUNCH(net, BP_K_CHANGE,
+              bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
+                                 wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk));
+    if (bpk::change_splits(net->n[l], net->n[l + 1], rows) > 1)
+      BP_LAUNCH(net, BP_K_SPLITK,
+                bpk::splitk_finish(s, net->n[l], net->n[l + 1], rows, wl(net, l), vl(net, l), net->ldw[l], lr, mom,
+                                   net->splitk));
+    BP_LAUNCH(net, BP_K_BIAS,
+              bpk::bias_update(s, net->del[l + 1], net->lda[l + 1], rows, net->n[l + 1], wbias(net, l),
+                               vbias(net, l), lr, mom));
   }
   return BP_OK;
 }
@@ -227,7 +274,7 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
     rc = run_backward_update(net, b, rows, lr, mom);
     if (rc) return rc;
   }
-  BP_HIP(net, bpk::sse_reduce(net->stream, net->sse_part, (int)used, net->sse_dev));
+  BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(net->stream, net->sse_part, (int)used, net->sse_dev));
   if (sse_out) {
     BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, net->stream));
     BP_HIP(net, hipStreamSynchronize(net->stream));
@@ -324,6 +371,11 @@ void bp_destroy(bp_net* net) {
   free_ptr(net->sse_dev);
   free_ptr(net->W);
   free_ptr(net->V);
+  for (auto& r : net->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : net->ev_pool) (void)hipEventDestroy(e);
   delete net;
 }
 
@@ -425,6 +477,45 @@ int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, 
   in.act = active_dev;
   in.n_active = n_active;
   return forward_only(net, in, n_patterns, outputs_dev);
+}
+
+int bp_profile(bp_net* net, int on) {
+  if (check_net(net)) return BP_EINVAL;
+  if (on) {
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+    for (auto& r : net->recs) {
+      net->ev_pool.push_back(r.a);
+      net->ev_pool.push_back(r.b);
+    }
+    net->recs.clear();
+    for (int k = 0; k < BP_K_COUNT; ++k) {
+      net->prof_n[k] = 0;
+      net->prof_ms[k] = 0.0;
+    }
+  }
+  net->prof = on != 0;
+  return BP_OK;
+}
+
+int bp_profile_report(bp_net* net, int64_t* launches, double* ms, int32_t n_kinds) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!launches || !ms || n_kinds < 0 || n_kinds > BP_K_COUNT)
+    return fail(net, BP_EINVAL, "bp_profile_report: bad output arrays");
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  for (auto& r : net->recs) {
+    float t = 0.f;
+    BP_HIP(net, hipEventElapsedTime(&t, r.a, r.b));
+    net->prof_n[r.kind] += 1;
+    net->prof_ms[r.kind] += (double)t;
+    net->ev_pool.push_back(r.a);
+    net->ev_pool.push_back(r.b);
+  }
+  net->recs.clear();
+  for (int k = 0; k < n_kinds; ++k) {
+    launches[k] = net->prof_n[k];
+    ms[k] = net->prof_ms[k];
+  }
+  return BP_OK;
 }
 
 const char* bp_last_error(const bp_net* net) { return net ? net->err.c_str() : g_create_err.c_str(); }
