@@ -50,7 +50,10 @@ KERNEL_NAMES = {
     "gather": "onehot_forward_kernel",
     "scatter": "onehot_update_kernel",
     "reduce": "sse_reduce_kernel",
+    "fused_fb": "small_fwdbwd_kernel",
+    "fused_update": "small_update_kernel",
 }
+SMALL_MAX_HIDDEN, SMALL_MAX_OUT, SMALL_MAX_ACTIVE = 256, 64, 32   # the library's fused-path limits
 
 
 def kind_work(sizes, rows, onehot, n_active, splits_of):
@@ -63,6 +66,13 @@ def kind_work(sizes, rows, onehot, n_active, splits_of):
 
     L = len(sizes) - 1
     R = float(rows)
+    if onehot and L == 2 and sizes[1] <= SMALL_MAX_HIDDEN and sizes[2] <= SMALL_MAX_OUT and n_active <= SMALL_MAX_ACTIVE:
+        n0, H, O = sizes
+        add("fused_fb", R * (H * (n_active + 1) + 4 * H * O),
+            4 * (R * n_active + (n0 + 1) * H + (H + 1) * O + R * O + 2 * R * H + R * O))
+        add("fused_update", R * (2 * (H + 1) * O + H * (n_active + 1)),
+            4 * (R * n_active + 2 * R * H + R * O) + 16 * ((n0 + 1) * H + (H + 1) * O))
+        return w
     for l in range(L):
         ni, no = sizes[l], sizes[l + 1]
         if l == 0 and onehot:

@@ -133,7 +133,9 @@ enum {
   BP_K_GATHER = 6,    /* one-hot first-layer forward                        */
   BP_K_SCATTER = 7,   /* one-hot first-layer change + momentum update       */
   BP_K_REDUCE = 8,    /* epoch error reduction                              */
-  BP_K_COUNT = 9
+  BP_K_FUSED_FB = 9,  /* small one-hot nets: whole forward + backward pass  */
+  BP_K_FUSED_UPD = 10,/* small one-hot nets: both layers' change + update   */
+  BP_K_COUNT = 11
 };
 
 /* on != 0: from now on every kernel launch of this net is bracketed by HIP

@@ -6,11 +6,35 @@
 // rounded up to a multiple of 4; row n_l is the bias ("true unit") row.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace bpk {
+
+// Measurement: when `start` is set, the next kernel launch of this thread
+// records its execution start and end on these events (taken from the
+// dispatch itself, hipExtLaunchKernel), then clears them and sets `used`.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+  bool used = false;
+};
+LaunchEvents& launch_events();
+
+template <class K, class... Args>
+hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t s, Args... args) {
+  LaunchEvents& ev = launch_events();
+  if (ev.start) {
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shmem, s, ev.start, ev.stop, 0u, args...);
+    ev.start = ev.stop = nullptr;
+    ev.used = true;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  }
+  return hipGetLastError();
+}
 
 // Number of blocks (and SSE partials) the output-layer forward launch uses.
 int output_delta_blocks(int M, int N);
@@ -67,6 +91,28 @@ hipError_t onehot_forward(hipStream_t s, const int32_t* act, int n_active, int r
 //   G[n0][j] = sum_p D[p][j];  V = lr G + mom V;  W += V.
 hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* D, int ldd,
                          int n0, int H, float* W, float* V, int ldw, float lr, float mom);
+
+// ---- fused path for small two-layer nets with one-hot inputs (bp_small.hip)
+constexpr int kSmallMaxHidden = 256;
+constexpr int kSmallMaxOut = 64;
+constexpr int kSmallMaxActive = 32;   // active inputs per pattern
+
+// True if a one-hot net n0 - H - O fits the fused path.
+bool small_path_fits(int n0, int H, int O, int n_active);
+
+// Number of blocks (and error partials) of small_fwdbwd for `rows` patterns.
+int small_fwdbwd_blocks(int rows);
+
+// Per pattern: A1 = sigma(W0 gather + bias), Y = sigma(A1 W1 + bias1),
+// D2 = (T - Y) Y (1 - Y), D1 = (D2 W1^T) A1 (1 - A1); error partials per block.
+hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
+                        int H, const float* W1, int ldw1, int O, const float* T, float* A1, int lda1, float* D1,
+                        float* D2, int ldd2, double* sse_part);
+
+// Summed changes of both layers over the batch and the momentum update of all weights.
+hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
+                        int lda1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
+                        float* V1, int ldw1, int O, float lr, float mom);
 
 // out[0] = sum of part[0 .. n-1] in a fixed order (double).
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out);

@@ -300,14 +300,16 @@ hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, i
   const bool bvec = (ldb % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) & 15) == 0);
   dim3 grid(tiles, 1, splits), block(kThreads);
   if (avec && bvec)
-    gemm_kernel<BM, BN, BK, A_KM, B_NK, true, true, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
-  else if (avec)
-    gemm_kernel<BM, BN, BK, A_KM, B_NK, true, false, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
-  else if (bvec)
-    gemm_kernel<BM, BN, BK, A_KM, B_NK, false, true, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
-  else
-    gemm_kernel<BM, BN, BK, A_KM, B_NK, false, false, Epi><<<grid, block, 0, s>>>(A, lda, B, ldb, M, N, K, k_chunk, epi);
-  return hipGetLastError();
+    return launch_kernel(gemm_kernel<BM, BN, BK, A_KM, B_NK, true, true, Epi>, grid, block, 0, s, A, lda, B, ldb, M,
+                         N, K, k_chunk, epi);
+  if (avec)
+    return launch_kernel(gemm_kernel<BM, BN, BK, A_KM, B_NK, true, false, Epi>, grid, block, 0, s, A, lda, B, ldb, M,
+                         N, K, k_chunk, epi);
+  if (bvec)
+    return launch_kernel(gemm_kernel<BM, BN, BK, A_KM, B_NK, false, true, Epi>, grid, block, 0, s, A, lda, B, ldb, M,
+                         N, K, k_chunk, epi);
+  return launch_kernel(gemm_kernel<BM, BN, BK, A_KM, B_NK, false, false, Epi>, grid, block, 0, s, A, lda, B, ldb, M, N,
+                       K, k_chunk, epi);
 }
 
 constexpr int kBM = 128, kBN = 128;
@@ -451,15 +453,22 @@ __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* 
   }
 }
 
-// Fixed-order sum of n doubles by one block.
-__global__ __launch_bounds__(kThreads) void sse_reduce_kernel(const double* __restrict__ part, int n,
-                                                              double* out) {
-  __shared__ double red[kThreads];
+// Fixed-order sum of n doubles by one block of 1024 threads: thread t adds
+// elements t, t + 1024, ... (loads issued eight at a time), then a tree.
+constexpr int kRed = 1024;
+__global__ __launch_bounds__(kRed) void sse_reduce_kernel(const double* __restrict__ part, int n, double* out) {
+  __shared__ double red[kRed];
   double s = 0.0;
-  for (int i = threadIdx.x; i < n; i += kThreads) s += part[i];
+  for (int i0 = threadIdx.x; i0 < n; i0 += 8 * kRed) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = i0 + u * kRed < n ? part[i0 + u * kRed] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int w = kThreads / 2; w > 0; w >>= 1) {
+  for (int w = kRed / 2; w > 0; w >>= 1) {
     if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
@@ -484,6 +493,11 @@ int chunk_for(int K, int splits) {
 
 // --------------------------------------------------------------------------
 // Launch wrappers (declared in bp_internal.h).
+
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
 
 int output_delta_blocks(int M, int N) { return ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN); }
 
@@ -534,16 +548,14 @@ hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V,
   if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
   const int ldp = (N + 3) / 4 * 4;
   const size_t total = (size_t)M * N;
-  splitk_update_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
+  return launch_kernel(splitk_update_kernel, (unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s, 
       ws, sp, (size_t)M * ldp, M, N, ldp, W, V, ldw, lr, mom);
-  return hipGetLastError();
 }
 
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb, float lr,
                        float mom) {
   if (N <= 0) return hipSuccess;
-  bias_update_kernel<<<(N + 63) / 64, 64 * kBiasWaves, 0, s>>>(D, ldd, rows, N, Wb, Vb, lr, mom);
-  return hipGetLastError();
+  return launch_kernel(bias_update_kernel, (N + 63) / 64, 64 * kBiasWaves, 0, s, D, ldd, rows, N, Wb, Vb, lr, mom);
 }
 
 int onehot_forward_blocks(int rows, int H) {
@@ -556,22 +568,19 @@ hipError_t onehot_forward(hipStream_t s, const int32_t* act, int n_active, int r
                           int n0, int H, int mode, float* out, int ldo, const float* T, int ldt, double* sse_part) {
   if (rows <= 0 || H <= 0) return hipSuccess;
   const int strips = (H + 63) / 64;
-  onehot_forward_kernel<<<onehot_forward_blocks(rows, H), kThreads, 0, s>>>(act, n_active, rows, W0, ldw, n0, H,
+  return launch_kernel(onehot_forward_kernel, onehot_forward_blocks(rows, H), kThreads, 0, s, act, n_active, rows, W0, ldw, n0, H,
                                                                             strips, mode, out, ldo, T, ldt, sse_part);
-  return hipGetLastError();
 }
 
 hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* D, int ldd, int n0,
                          int H, float* W, float* V, int ldw, float lr, float mom) {
   if (H <= 0) return hipSuccess;
   dim3 grid(n0 + 1, (H + kThreads - 1) / kThreads);
-  onehot_update_kernel<<<grid, kThreads, 0, s>>>(act, n_active, rows, D, ldd, n0, H, W, V, ldw, lr, mom);
-  return hipGetLastError();
+  return launch_kernel(onehot_update_kernel, grid, kThreads, 0, s, act, n_active, rows, D, ldd, n0, H, W, V, ldw, lr, mom);
 }
 
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out) {
-  sse_reduce_kernel<<<1, kThreads, 0, s>>>(part, n, out);
-  return hipGetLastError();
+  return launch_kernel(sse_reduce_kernel, 1, kRed, 0, s, part, n, out);
 }
 
 }  // namespace bpk

@@ -91,16 +91,26 @@ hipEvent_t take_event(bp_net* net) {
   return e;
 }
 
-// Runs one launch; while profiling, brackets it with events on the stream.
+// Runs one launch; while profiling, the kernel records its execution start
+// and end (from its own dispatch) on a pair of events.
 template <class F>
 hipError_t launch(bp_net* net, int kind, F&& f) {
   if (!net->prof) return f();
   hipEvent_t a = take_event(net), b = take_event(net);
   if (!a || !b) return hipErrorOutOfMemory;
-  hipError_t e = hipEventRecord(a, net->stream);
-  if (e == hipSuccess) e = f();
-  if (e == hipSuccess) e = hipEventRecord(b, net->stream);
-  net->recs.push_back({kind, a, b});
+  bpk::LaunchEvents& ev = bpk::launch_events();
+  ev.start = a;
+  ev.stop = b;
+  ev.used = false;
+  const hipError_t e = f();
+  const bool used = ev.used;
+  ev = bpk::LaunchEvents();
+  if (used) {
+    net->recs.push_back({kind, a, b});
+  } else {
+    net->ev_pool.push_back(a);
+    net->ev_pool.push_back(b);
+  }
   return e;
 }
 
@@ -211,9 +221,29 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
   return BP_OK;
 }
 
+// One-hot two-layer nets small enough for the fused two-launch update.
+bool use_small(const bp_net* net, const BatchInput& in) {
+  return in.act && net->L == 2 && bpk::small_path_fits(net->n[0], net->n[1], net->n[2], in.n_active);
+}
+
 int sse_blocks(const bp_net* net, const BatchInput& in, int rows) {
+  if (use_small(net, in)) return bpk::small_fwdbwd_blocks(rows);
   if (net->L == 1 && in.act) return bpk::onehot_forward_blocks(rows, net->n[1]);
   return bpk::output_delta_blocks(rows, net->n[net->L]);
+}
+
+// One pooled update of a small one-hot two-layer net: two launches.
+int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part, float lr, float mom) {
+  hipStream_t s = net->stream;
+  const int n0 = net->n[0], H = net->n[1], O = net->n[2];
+  BP_LAUNCH(net, BP_K_FUSED_FB,
+            bpk::small_fwdbwd(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], n0, H, wl(net, 1), net->ldw[1], O,
+                              T, net->act[1], net->lda[1], net->del[1], net->del[2], net->lda[2], sse_part));
+  BP_LAUNCH(net, BP_K_FUSED_UPD,
+            bpk::small_update(s, in.act, in.n_active, rows, net->act[1], net->del[1], net->lda[1], net->del[2],
+                              net->lda[2], wl(net, 0), vl(net, 0), net->ldw[0], n0, H, wl(net, 1), vl(net, 1),
+                              net->ldw[1], O, lr, mom));
+  return BP_OK;
 }
 
 // Backward pass and update of one batch whose deltas of the output layer are
@@ -257,9 +287,12 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
   const int64_t rows_max = std::min<int64_t>(batch, n);
   int rc = ensure_workspace(net, rows_max);
   if (rc) return rc;
+  // exact number of error partials: every batch but the last has rows_max rows
   const int64_t nb = (n + batch - 1) / batch;
-  const size_t per = (size_t)sse_blocks(net, in, (int)rows_max);
-  rc = ensure_sse(net, per * (size_t)nb);
+  const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
+  const size_t need = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +
+                      (size_t)sse_blocks(net, in, last_rows);
+  rc = ensure_sse(net, need);
   if (rc) return rc;
   size_t used = 0;
   for (int64_t p0 = 0; p0 < n; p0 += batch) {
@@ -267,8 +300,14 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
     BatchInput b = in;
     if (b.x) b.x += (size_t)p0 * net->n[0];
     if (b.act) b.act += (size_t)p0 * b.n_active;
-    rc = run_forward(net, b, rows, targets + (size_t)p0 * net->n[net->L], net->sse_part + used, nullptr, 0,
-                     net->act.data());
+    const float* Tb = targets + (size_t)p0 * net->n[net->L];
+    if (use_small(net, b)) {
+      rc = run_small(net, b, rows, Tb, net->sse_part + used, lr, mom);
+      if (rc) return rc;
+      used += (size_t)sse_blocks(net, b, rows);
+      continue;
+    }
+    rc = run_forward(net, b, rows, Tb, net->sse_part + used, nullptr, 0, net->act.data());
     if (rc) return rc;
     used += (size_t)sse_blocks(net, b, rows);
     rc = run_backward_update(net, b, rows, lr, mom);

@@ -120,6 +120,10 @@ def test_first_update_full_size(dev, name):
     ((203, 300, 26), 600, 300, True),
     ((20, 4), 9, 9, True),
     ((1030, 260, 70), 1100, 1100, False),
+    ((203, 120, 26), 255, 128, True),     # fused path: short last batch needs more blocks than a full one
+    ((203, 256, 64), 300, 100, True),     # fused path at its largest hidden and output sizes
+    ((60, 1, 1), 40, 7, True),
+    ((203, 257, 26), 70, 70, True),       # just past the fused path's hidden limit (generic path)
 ])
 def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
