@@ -52,6 +52,7 @@ KERNEL_NAMES = {
     "reduce": "sse_reduce_kernel",
     "fused_fb": "small_fwdbwd_kernel",
     "fused_update": "small_update_kernel",
+    "output_finish": "output_finish_kernel",
 }
 SMALL_MAX_HIDDEN, SMALL_MAX_OUT, SMALL_MAX_ACTIVE = 256, 64, 32   # the library's fused-path limits
 
@@ -79,7 +80,10 @@ def kind_work(sizes, rows, onehot, n_active, splits_of):
             add("gather", R * no * (n_active + 1), 4 * (R * n_active + (ni + 1) * no + R * no))
             add("scatter", R * no * (n_active + 1), 4 * (R * n_active + R * no) + 16 * (ni + 1) * no)
         else:
-            if l == L - 1:
+            if l == L - 1 and splits_of(rows, no, ni) > 1:
+                add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no))
+                add("output_finish", 6 * R * no, 4 * (2 * R * no + no))
+            elif l == L - 1:
                 add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + 2 * R * no))
             else:
                 add("forward", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + R * no))
@@ -89,7 +93,7 @@ def kind_work(sizes, rows, onehot, n_active, splits_of):
                 add("splitk", 0.0, upd)
             else:
                 add("change", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
-            add("bias", R * no, 4 * R * no + 16 * no)
+            add("bias", R * no, 4 * -(-rows // 128) * no + 16 * no)
         if l >= 1:
             add("backward", 2 * R * no * ni, 4 * (R * no + ni * no + 2 * R * ni))
     return w
@@ -98,9 +102,9 @@ def kind_work(sizes, rows, onehot, n_active, splits_of):
 def choose_splits(M, N, K):
     """Mirror of the library's split-K choice (128 x 128 tiles), for work accounting only."""
     tiles = -(-M // 128) * -(-N // 128)
-    if K < 1024 or tiles >= 128:
+    if K < 1024 or tiles >= 512:
         return 1
-    s = -(-256 // tiles)
+    s = -(-512 // tiles)
     return max(1, min(s, K // 256))
 
 

@@ -135,7 +135,8 @@ enum {
   BP_K_REDUCE = 8,    /* epoch error reduction                              */
   BP_K_FUSED_FB = 9,  /* small one-hot nets: whole forward + backward pass  */
   BP_K_FUSED_UPD = 10,/* small one-hot nets: both layers' change + update   */
-  BP_K_COUNT = 11
+  BP_K_OUTFIN = 11,   /* split-K output layer: partial sums + deltas + error */
+  BP_K_COUNT = 12
 };
 
 /* on != 0: from now on every kernel launch of this net is bracketed by HIP

@@ -26,7 +26,7 @@ EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set
            "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
            "bp_forward_onehot", "bp_profile", "bp_profile_report", "bp_last_error")
 KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce", "fused_fb",
-         "fused_update")
+         "fused_update", "output_finish")
 
 _lib = None
 _vp = ctypes.c_void_p

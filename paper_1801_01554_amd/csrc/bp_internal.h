@@ -36,8 +36,8 @@ hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, size_t shmem, hipStrea
   return hipGetLastError();
 }
 
-// Number of blocks (and SSE partials) the output-layer forward launch uses.
-int output_delta_blocks(int M, int N);
+// Rows of the per-tile column sums a delta-producing launch over M rows writes.
+int colsum_rows(int M);
 
 // out[m][n] = sigma(sum_k A[m][k] W[k][n] + bias[n]),  m < M, n < N, k < K.
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
@@ -45,15 +45,24 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
 
 // Output layer during training: y = sigma(A W + bias); e = T - y;
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of
-// block b (b < output_delta_blocks(M, N)).
+// block b (b < output_delta_blocks(M, N, K)); colsum[t][n] = sum of delta
+// over rows [128 t, 128 t + 128) (t < colsum_rows(M)).  With
+// output_delta_splits(M, N, K) > 1 the product writes split partials to `ws`
+// (output_delta_workspace floats) and output_finish applies the epilogue.
+int output_delta_blocks(int M, int N, int K);
+int output_delta_splits(int M, int N, int K);
+size_t output_delta_workspace(int M, int N, int K);
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M,
                                 int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                                int ldd, double* sse_part);
+                                int ldd, double* sse_part, float* colsum, int ldcs, float* ws);
+hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws);
 
 // Hidden deltas: out[m][n] = (sum_k D[m][k] W[n][k]) * act[m][n] (1 - act[m][n]),
-// with W rows n < N the non-bias rows of the layer above (ldw floats apart).
+// with W rows n < N the non-bias rows of the layer above (ldw floats apart);
+// colsum as for the output layer.
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N,
-                          int K, const float* act, int lda, float* out, int ldo);
+                          int K, const float* act, int lda, float* out, int ldo, float* colsum, int ldcs);
 
 // Number of K-splits change_update uses for an M x N change summed over K
 // rows (1 = the product applies the update itself).
@@ -74,6 +83,7 @@ hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V,
                          const float* ws);
 
 // Bias-row change and update: G[n] = sum_{k < rows} D[k][n];  V = lr G + mom V;  W += V.
+// D is the per-tile column-sum buffer of the deltas (rows = colsum_rows(batch)).
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb,
                        float lr, float mom);
 

@@ -28,17 +28,22 @@ __device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(
 
 // --------------------------------------------------------------------------
 // Epilogues.  apply() gets one element of the product (row m, column n) plus
-// the per-column value column() returned; kSSE marks epilogues that add to a
-// per-block squared-error partial.
+// the per-column value column() returned, and returns the value that enters
+// the per-tile column sums; kSSE marks epilogues that add to a per-block
+// squared-error partial, kColSum those that write per-tile column sums of
+// the deltas they produce (colsum[tile row][n]; the bias-row change of the
+// layer below is the sum of these over the tile rows).
 
 struct EpiSigmoid {
   const float* bias;
   float* out;
   int ldo;
   static constexpr bool kSSE = false;
+  static constexpr bool kColSum = false;
   __device__ float column(int n) const { return bias[n]; }
-  __device__ void apply(int m, int n, float acc, float b, float&) const {
+  __device__ float apply(int m, int n, float acc, float b, float&) const {
     out[(size_t)m * ldo + n] = logistic(acc + b);
+    return 0.f;
   }
 };
 
@@ -49,13 +54,18 @@ struct EpiOutputDelta {
   float* delta;
   int ldd;
   double* sse_part;
+  float* colsum;
+  int ldcs;
   static constexpr bool kSSE = true;
+  static constexpr bool kColSum = true;
   __device__ float column(int n) const { return bias[n]; }
-  __device__ void apply(int m, int n, float acc, float b, float& sse) const {
+  __device__ float apply(int m, int n, float acc, float b, float& sse) const {
     const float y = logistic(acc + b);
     const float e = T[(size_t)m * ldt + n] - y;
     sse += e * e;
-    delta[(size_t)m * ldd + n] = e * y * (1.0f - y);
+    const float d = e * y * (1.0f - y);
+    delta[(size_t)m * ldd + n] = d;
+    return d;
   }
 };
 
@@ -64,11 +74,16 @@ struct EpiHiddenDelta {
   int lda;
   float* out;
   int ldo;
+  float* colsum;
+  int ldcs;
   static constexpr bool kSSE = false;
+  static constexpr bool kColSum = true;
   __device__ float column(int) const { return 0.f; }
-  __device__ void apply(int m, int n, float acc, float, float&) const {
+  __device__ float apply(int m, int n, float acc, float, float&) const {
     const float a = act[(size_t)m * lda + n];
-    out[(size_t)m * ldo + n] = acc * (a * (1.0f - a));
+    const float d = acc * (a * (1.0f - a));
+    out[(size_t)m * ldo + n] = d;
+    return d;
   }
 };
 
@@ -78,12 +93,14 @@ struct EpiUpdate {
   int ldw;
   float lr, mom;
   static constexpr bool kSSE = false;
+  static constexpr bool kColSum = false;
   __device__ float column(int) const { return 0.f; }
-  __device__ void apply(int m, int n, float acc, float, float&) const {
+  __device__ float apply(int m, int n, float acc, float, float&) const {
     const size_t i = (size_t)m * ldw + n;
     const float v = lr * acc + mom * V[i];
     V[i] = v;
     W[i] = W[i] + v;
+    return 0.f;
   }
 };
 
@@ -93,9 +110,11 @@ struct EpiPartial {
   int ldp;
   size_t split_stride;
   static constexpr bool kSSE = false;
+  static constexpr bool kColSum = false;
   __device__ float column(int) const { return 0.f; }
-  __device__ void apply(int m, int n, float acc, float, float&) const {
+  __device__ float apply(int m, int n, float acc, float, float&) const {
     P[blockIdx.z * split_stride + (size_t)m * ldp + n] = acc;
+    return 0.f;
   }
 };
 
@@ -150,6 +169,19 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld
   }
 }
 
+// Loads a TO x TD tile that lies entirely inside the matrix, 16 bytes per
+// load, with no bounds checks (interior tiles of 16-byte aligned operands).
+template <int TO, int TD>
+__device__ __forceinline__ void load_tile_full(const float* __restrict__ base, int ld, int o0, int d0, f32x4* r) {
+  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int D4 = TD / 4;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int f = threadIdx.x + q * kThreads;
+    r[q] = *reinterpret_cast<const f32x4*>(base + (size_t)(o0 + f / D4) * ld + d0 + (f % D4) * 4);
+  }
+}
+
 template <int TO, int TD, int S>
 __device__ __forceinline__ void store_tile(float* lds, const f32x4* r) {
   constexpr int PER = TO * TD / 4 / kThreads;
@@ -197,11 +229,24 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   f32x4 ra[T::LA], rb[T::LB];
+  // Interior tiles (the block-uniform common case) take the unchecked path.
+  const bool a_rows_in = m0 + BM <= M, b_rows_in = n0 + BN <= N;
   auto load_stage = [&](int k) {
-    if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra);
-    else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra);
-    if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb);
-    else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb);
+    const bool k_in = k + BK <= ke;
+    if (AVEC && a_rows_in && k_in) {
+      if (A_KM) load_tile_full<BK, BM>(A, lda, k, m0, ra);
+      else load_tile_full<BM, BK>(A, lda, m0, k, ra);
+    } else {
+      if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra);
+      else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra);
+    }
+    if (BVEC && b_rows_in && k_in) {
+      if (B_NK) load_tile_full<BN, BK>(B, ldb, n0, k, rb);
+      else load_tile_full<BK, BN>(B, ldb, k, n0, rb);
+    } else {
+      if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb);
+      else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb);
+    }
   };
   auto store_stage = [&](int buf) {
     if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra);
@@ -259,8 +304,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
   float sse = 0.f;
+  float csum[T::TN];
 #pragma unroll
   for (int j = 0; j < T::TN; ++j) {
+    csum[j] = 0.f;
     const int n = n0 + wn0 + j * 32 + r;
     if (n < N) {
       const float cv = epi.column(n);
@@ -269,10 +316,23 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-          if (m < M) epi.apply(m, n, acc[i][j][e], cv, sse);
+          if (m < M) csum[j] += epi.apply(m, n, acc[i][j][e], cv, sse);
         }
       }
     }
+  }
+  if constexpr (Epi::kColSum) {
+    // lanes h = 0, 1 hold the same column (different rows); then the two
+    // waves stacked in M are added in a fixed order.
+    __shared__ float cs[2][BN];
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j) {
+      const float v = csum[j] + __shfl_xor(csum[j], 32, 64);
+      if (h == 0) cs[wave >> 1][wn0 + j * 32 + r] = v;
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < BN; c += kThreads)
+      if (n0 + c < N) epi.colsum[(size_t)(tile / tiles_n) * epi.ldcs + n0 + c] = cs[0][c] + cs[1][c];
   }
   if constexpr (Epi::kSSE) {
     __shared__ float red[kThreads / 64];
@@ -329,6 +389,66 @@ __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __
   const float v = lr * g + mom * V[i];
   V[i] = v;
   W[i] = W[i] + v;
+}
+
+// Split-K output layer: sums the split partials in split order, then applies
+// the output-delta epilogue (bias, sigma, e = T - y, delta = e y (1 - y)).
+// Block (x, y) covers rows [128 x, 128 x + 128) and columns [64 y, 64 y + 64)
+// with 16 waves; lane = column, wave w = rows 8 w .. 8 w + 7 (their loads
+// issued together).  Writes the block's error partial and the 128-row column
+// sums of the deltas (the tiling of the fused epilogue), both in wave order.
+constexpr int kFin = 1024;
+__global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __restrict__ P, int splits, size_t stride,
+                                                             int ldp, int M, int N, const float* __restrict__ bias,
+                                                             const float* __restrict__ T, int ldt, float* delta,
+                                                             int ldd, double* sse_part, float* colsum, int ldcs) {
+  constexpr int W = kFin / 64, R = 128 / W;
+  __shared__ float cs[W][64];
+  __shared__ float red[W];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = blockIdx.y * 64 + lane;
+  const int m0 = blockIdx.x * 128 + wave * R;
+  float sse = 0.f, csum = 0.f;
+  if (n < N) {
+    const float b = bias[n];
+    float z[R], t[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      z[r] = 0.f;
+      t[r] = m0 + r < M ? T[(size_t)(m0 + r) * ldt + n] : 0.f;
+    }
+    for (int sp = 0; sp < splits; ++sp) {
+      float v[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) v[r] = m0 + r < M ? P[sp * stride + (size_t)(m0 + r) * ldp + n] : 0.f;
+#pragma unroll
+      for (int r = 0; r < R; ++r) z[r] += v[r];
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (m0 + r >= M) break;
+      const float y = logistic(z[r] + b);
+      const float e = t[r] - y;
+      sse += e * e;
+      const float d = e * y * (1.0f - y);
+      delta[(size_t)(m0 + r) * ldd + n] = d;
+      csum += d;
+    }
+  }
+  cs[wave][lane] = csum;
+  for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+  if (lane == 0) red[wave] = sse;
+  __syncthreads();
+  if (wave == 0 && n < N) {
+    float c = cs[0][lane];
+    for (int w = 1; w < W; ++w) c += cs[w][lane];
+    colsum[(size_t)blockIdx.x * ldcs + n] = c;
+  }
+  if (threadIdx.x == 0) {
+    double tt = 0.0;
+    for (int w = 0; w < W; ++w) tt += (double)red[w];
+    sse_part[blockIdx.y * gridDim.x + blockIdx.x] = tt;
+  }
 }
 
 // Bias-row change: column sums of D over `rows` rows, then the update.  Block
@@ -475,14 +595,18 @@ __global__ __launch_bounds__(kRed) void sse_reduce_kernel(const double* __restri
   if (threadIdx.x == 0) out[0] = red[0];
 }
 
+// K-splits for a product with few output tiles: enough blocks for two per
+// CU (512), each split at least 256 deep in K.
 int choose_splits(int M, int N, int K) {
   const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  if (K < 1024 || tiles >= 128) return 1;
-  int s = (256 + tiles - 1) / tiles;
+  if (K < 1024 || tiles >= 512) return 1;
+  int s = (512 + tiles - 1) / tiles;
   const int max_s = K / 256;
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;
 }
+
+int choose_output_splits(int M, int N, int K) { return choose_splits(M, N, K); }
 
 int chunk_for(int K, int splits) {
   int c = (K + splits - 1) / splits;
@@ -499,7 +623,20 @@ LaunchEvents& launch_events() {
   return ev;
 }
 
-int output_delta_blocks(int M, int N) { return ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN); }
+int colsum_rows(int M) { return (M + kBM - 1) / kBM; }
+
+int output_delta_blocks(int M, int N, int K) {
+  if (choose_output_splits(M, N, K) > 1) return ((M + 127) / 128) * ((N + 63) / 64);
+  return ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+}
+
+size_t output_delta_workspace(int M, int N, int K) {
+  const int sp = choose_output_splits(M, N, K);
+  if (sp <= 1) return 0;
+  return (size_t)sp * M * ((N + 3) / 4 * 4);
+}
+
+int output_delta_splits(int M, int N, int K) { return choose_output_splits(M, N, K); }
 
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
                          const float* bias, float* out, int ldo) {
@@ -507,16 +644,32 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
   return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
 }
 
-hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
-                                int K, const float* bias, const float* T, int ldt, float* delta, int ldd,
-                                double* sse_part) {
-  EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part};
-  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
+                                const float* bias, const float* T, int ldt, float* delta, int ldd, double* sse_part,
+                                float* colsum, int ldcs, float* ws) {
+  const int sp = choose_output_splits(M, N, K);
+  if (sp <= 1) {
+    EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs};
+    return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+  }
+  const int ldp = (N + 3) / 4 * 4;
+  EpiPartial e{ws, ldp, (size_t)M * ldp};
+  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, sp, chunk_for(K, sp), e);
+}
+
+hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws) {
+  const int sp = choose_output_splits(M, N, K);
+  if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
+  const int ldp = (N + 3) / 4 * 4;
+  dim3 grid((M + 127) / 128, (N + 63) / 64);
+  return launch_kernel(output_finish_kernel, grid, kFin, 0, s, ws, sp, (size_t)M * ldp, ldp, M, N, bias, T, ldt,
+                       delta, ldd, sse_part, colsum, ldcs);
 }
 
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,
-                          const float* act, int lda, float* out, int ldo) {
-  EpiHiddenDelta e{act, lda, out, ldo};
+                          const float* act, int lda, float* out, int ldo, float* colsum, int ldcs) {
+  EpiHiddenDelta e{act, lda, out, ldo, colsum, ldcs};
   return launch_gemm<kBM, kBN, false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 

@@ -35,6 +35,7 @@ struct bp_net {
   int64_t ws_rows = 0;
   std::vector<float*> act;            // act[l], l = 1 .. L-1 : [ws_rows][lda[l]]
   std::vector<float*> del;            // del[l], l = 1 .. L   : [ws_rows][lda[l]]
+  std::vector<float*> csum;           // csum[l], l = 1 .. L  : [colsum_rows(ws_rows)][lda[l]]
   float* fwd_tmp[2] = {nullptr, nullptr};  // forward-only ping-pong buffers
   int64_t fwd_rows = 0;
   size_t fwd_cap = 0;
@@ -123,8 +124,10 @@ void free_ptr(void* p) {
 void free_workspace(bp_net* net) {
   for (float* p : net->act) free_ptr(p);
   for (float* p : net->del) free_ptr(p);
+  for (float* p : net->csum) free_ptr(p);
   net->act.assign(net->L + 1, nullptr);
   net->del.assign(net->L + 1, nullptr);
+  net->csum.assign(net->L + 1, nullptr);
   net->ws_rows = 0;
   free_ptr(net->splitk);
   net->splitk = nullptr;
@@ -139,8 +142,10 @@ int ensure_workspace(bp_net* net, int64_t rows) {
     const size_t bytes = sizeof(float) * (size_t)rows * net->lda[l];
     if (l < net->L) BP_HIP(net, hipMalloc(&net->act[l], bytes));
     BP_HIP(net, hipMalloc(&net->del[l], bytes));
+    BP_HIP(net, hipMalloc(&net->csum[l], sizeof(float) * (size_t)bpk::colsum_rows((int)rows) * net->lda[l]));
   }
-  size_t sk = 0;
+  // split-K partials: the output layer's and every change product's (used one at a time)
+  size_t sk = bpk::output_delta_workspace((int)rows, net->n[net->L], net->n[net->L - 1]);
   for (int l = 0; l < net->L; ++l)
     sk = std::max(sk, bpk::change_update_workspace(net->n[l], net->n[l + 1], (int)rows));
   if (sk) BP_HIP(net, hipMalloc(&net->splitk, sizeof(float) * sk));
@@ -209,11 +214,16 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
     }
     const float* A = (l == 0) ? in.x : acts[l];
     const int ldA = (l == 0) ? net->n[0] : net->lda[l];
-    if (last && T)
+    if (last && T) {
       BP_LAUNCH(net, BP_K_OUTPUT,
                 bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
-                                          wbias(net, l), T, net->n[L], dst, ldd, sse_part));
-    else
+                                          wbias(net, l), T, net->n[L], dst, ldd, sse_part, net->csum[L],
+                                          net->lda[L], net->splitk));
+      if (bpk::output_delta_splits(rows, net->n[l + 1], net->n[l]) > 1)
+        BP_LAUNCH(net, BP_K_OUTFIN,
+                  bpk::output_finish(s, rows, net->n[l + 1], net->n[l], wbias(net, l), T, net->n[L], dst, ldd,
+                                     sse_part, net->csum[L], net->lda[L], net->splitk));
+    } else
       BP_LAUNCH(net, BP_K_FORWARD,
                 bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
                                    wbias(net, l), dst, ldd));
@@ -229,7 +239,7 @@ bool use_small(const bp_net* net, const BatchInput& in) {
 int sse_blocks(const bp_net* net, const BatchInput& in, int rows) {
   if (use_small(net, in)) return bpk::small_fwdbwd_blocks(rows);
   if (net->L == 1 && in.act) return bpk::onehot_forward_blocks(rows, net->n[1]);
-  return bpk::output_delta_blocks(rows, net->n[net->L]);
+  return bpk::output_delta_blocks(rows, net->n[net->L], net->n[net->L - 1]);
 }
 
 // One pooled update of a small one-hot two-layer net: two launches.
@@ -255,7 +265,8 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
     if (l >= 1)
       BP_LAUNCH(net, BP_K_BACKWARD,
                 bpk::backward_layer(s, net->del[l + 1], net->lda[l + 1], wl(net, l), net->ldw[l], rows, net->n[l],
-                                    net->n[l + 1], net->act[l], net->lda[l], net->del[l], net->lda[l]));
+                                    net->n[l + 1], net->act[l], net->lda[l], net->del[l], net->lda[l], net->csum[l],
+                                    net->lda[l]));
     if (l == 0 && in.act) {
       BP_LAUNCH(net, BP_K_SCATTER,
                 bpk::onehot_update(s, in.act, in.n_active, rows, net->del[1], net->lda[1], net->n[0], net->n[1],
@@ -272,8 +283,8 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
                 bpk::splitk_finish(s, net->n[l], net->n[l + 1], rows, wl(net, l), vl(net, l), net->ldw[l], lr, mom,
                                    net->splitk));
     BP_LAUNCH(net, BP_K_BIAS,
-              bpk::bias_update(s, net->del[l + 1], net->lda[l + 1], rows, net->n[l + 1], wbias(net, l),
-                               vbias(net, l), lr, mom));
+              bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1], bpk::colsum_rows(rows), net->n[l + 1],
+                               wbias(net, l), vbias(net, l), lr, mom));
   }
   return BP_OK;
 }
@@ -383,6 +394,7 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
   }
   net->act.assign(net->L + 1, nullptr);
   net->del.assign(net->L + 1, nullptr);
+  net->csum.assign(net->L + 1, nullptr);
   hipError_t e = hipGetDevice(&net->device);
   if (e == hipSuccess) e = hipMalloc(&net->W, sizeof(float) * net->wtotal);
   if (e == hipSuccess) e = hipMalloc(&net->V, sizeof(float) * net->wtotal);
