@@ -193,13 +193,21 @@ __device__ __forceinline__ void store_tile(float* lds, const f32x4* r) {
   }
 }
 
-// Maps the hardware block index to a tile so that the blocks one XCD receives
-// (hardware index mod 8) are consecutive tiles of the same tile row: they
-// share their A tiles in that XCD's L2.
-__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
+// Maps the hardware block index to a tile.  Blocks reach the eight XCDs
+// round-robin (hardware index mod 8); each XCD is given a contiguous range
+// of the tile order, and the tile order walks groups of 8 tile rows column by
+// column, so the blocks an XCD runs at once cover about 8 x 8 tiles and
+// share both their A and their B tiles in that XCD's L2.
+constexpr int kGroupM = 8;
+__device__ __forceinline__ void xcd_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int per = nblocks >> 3;
-  if (bid >= (per << 3)) return bid;
-  return (bid & 7) * per + (bid >> 3);
+  const int t = bid >= (per << 3) ? bid : (bid & 7) * per + (bid >> 3);
+  const int band = t / (kGroupM * tiles_n);
+  const int first = band * kGroupM;
+  const int rows = min(tiles_m - first, kGroupM);
+  const int in_band = t - band * kGroupM * tiles_n;
+  tm = first + in_band % rows;
+  tn = in_band / rows;
 }
 
 template <int BM, int BN, int BK, bool A_KM, bool B_NK, bool AVEC, bool BVEC, class Epi>
@@ -210,9 +218,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   __shared__ __attribute__((aligned(16))) float As[2][T::A_ELEMS];
   __shared__ __attribute__((aligned(16))) float Bs[2][T::B_ELEMS];
 
-  const int tiles_n = (N + BN - 1) / BN;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int tiles_n = (N + BN - 1) / BN, tiles_m = (M + BM - 1) / BM;
+  int tm, tn;
+  xcd_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
   const int kb = blockIdx.z * k_chunk;
   const int ke = min(K, kb + k_chunk);
 
@@ -228,10 +237,13 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  f32x4 ra[T::LA], rb[T::LB];
+  // Two register sets: the tile of stage s + 2 is loaded while stage s is
+  // multiplied, so a global load has two stages of MFMA work to land before
+  // its registers are written to LDS.
+  f32x4 ra0[T::LA], rb0[T::LB], ra1[T::LA], rb1[T::LB];
   // Interior tiles (the block-uniform common case) take the unchecked path.
   const bool a_rows_in = m0 + BM <= M, b_rows_in = n0 + BN <= N;
-  auto load_stage = [&](int k) {
+  auto load_stage = [&](int k, f32x4* ra, f32x4* rb) {
     const bool k_in = k + BK <= ke;
     if (AVEC && a_rows_in && k_in) {
       if (A_KM) load_tile_full<BK, BM>(A, lda, k, m0, ra);
@@ -248,24 +260,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb);
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int buf, const f32x4* ra, const f32x4* rb) {
     if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra);
     else store_tile<BM, BK, T::SA>(As[buf], ra);
     if (B_NK) store_tile<BN, BK, T::SB>(Bs[buf], rb);
     else store_tile<BK, BN, T::SB>(Bs[buf], rb);
   };
-
-  const int nst = ke > kb ? (ke - kb + BK - 1) / BK : 0;
-  if (nst > 0) {
-    load_stage(kb);
-    store_stage(0);
-    __syncthreads();
-  }
-  for (int s = 0; s < nst; ++s) {
-    const int cur = s & 1;
-    if (s + 1 < nst) load_stage(kb + (s + 1) * BK);
-    const float* as = As[cur];
-    const float* bs = Bs[cur];
+  auto compute = [&](int buf) {
+    const float* as = As[buf];
+    const float* bs = Bs[buf];
 #pragma unroll
     for (int g = 0; g < BK / 8; ++g) {
       f32x4 af[T::TM], bf[T::TN];
@@ -297,9 +300,29 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
           for (int j = 0; j < T::TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][t], bf[j][t], acc[i][j], 0, 0, 0);
     }
-    if (s + 1 < nst) store_stage(cur ^ 1);
+  };
+  // One pipeline step at stage s: registers `rl` (which held stage s, already
+  // in LDS) receive stage s + 2; LDS buffer s % 2 is multiplied; registers
+  // `rs` (stage s + 1) are written to the other LDS buffer.
+  const int nst = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+  auto step = [&](int s, f32x4* rla, f32x4* rlb, const f32x4* rsa, const f32x4* rsb) {
+    if (s + 2 < nst) load_stage(kb + (s + 2) * BK, rla, rlb);
+    compute(s & 1);
+    if (s + 1 < nst) store_stage((s + 1) & 1, rsa, rsb);
+    __syncthreads();
+  };
+  if (nst > 0) {
+    load_stage(kb, ra0, rb0);
+    if (nst > 1) load_stage(kb + BK, ra1, rb1);
+    store_stage(0, ra0, rb0);
     __syncthreads();
   }
+  int s = 0;
+  for (; s + 1 < nst; s += 2) {
+    step(s, ra0, rb0, ra1, rb1);       // even stage: loads s + 2 into set 0, stores set 1 (stage s + 1)
+    step(s + 1, ra1, rb1, ra0, rb0);   // odd stage: loads s + 3 into set 1, stores set 0 (stage s + 2)
+  }
+  if (s < nst) step(s, ra0, rb0, ra1, rb1);
 
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
@@ -322,8 +345,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
     }
   }
   if constexpr (Epi::kColSum) {
-    // lanes h = 0, 1 hold the same column (different rows); then the two
-    // waves stacked in M are added in a fixed order.
+    // Column sums per 128-row group of the tile.  Lanes h = 0, 1 hold the
+    // same column (different rows); the wave rows of a group are then added
+    // in a fixed order.
+    constexpr int kGroups = BM / 128, kWaveRowsPerGroup = 256 / BM;
     __shared__ float cs[2][BN];
 #pragma unroll
     for (int j = 0; j < T::TN; ++j) {
@@ -331,8 +356,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       if (h == 0) cs[wave >> 1][wn0 + j * 32 + r] = v;
     }
     __syncthreads();
-    for (int c = threadIdx.x; c < BN; c += kThreads)
-      if (n0 + c < N) epi.colsum[(size_t)(tile / tiles_n) * epi.ldcs + n0 + c] = cs[0][c] + cs[1][c];
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+      const int crow = tm * kGroups + g;
+      if (crow * 128 >= M) break;
+      for (int c = threadIdx.x; c < BN; c += kThreads) {
+        if (n0 + c >= N) continue;
+        float v = cs[g * kWaveRowsPerGroup][c];
+        for (int w = 1; w < kWaveRowsPerGroup; ++w) v += cs[g * kWaveRowsPerGroup + w][c];
+        epi.colsum[(size_t)crow * epi.ldcs + n0 + c] = v;
+      }
+    }
   }
   if constexpr (Epi::kSSE) {
     __shared__ float red[kThreads / 64];
@@ -348,10 +382,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   }
 }
 
-// Tile configurations.
-constexpr int BK = 32;
+// Tile configuration: 128 x 128 x 32, wave tile 64 x 64, two blocks per CU
+// (72 KB of LDS with both buffers).  (A 256 x 128 x 16 tile, one block per
+// CU round for more products, measured slower on the wide and deep nets.)
+constexpr int kTileM = 128, kTileN = 128, kTileK = 32;
+constexpr int kChunkAlign = kTileK;   // split-K chunks are multiples of BK
 
-template <int BM, int BN, bool A_KM, bool B_NK, class Epi>
+inline int tile_count(int M, int N) { return ((M + kTileM - 1) / kTileM) * ((N + kTileN - 1) / kTileN); }
+
+template <int BM, int BN, int BK, bool A_KM, bool B_NK, class Epi>
 hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
                        int splits, int k_chunk, const Epi& epi) {
   if (M <= 0 || N <= 0) return hipSuccess;
@@ -372,7 +411,11 @@ hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, i
                        K, k_chunk, epi);
 }
 
-constexpr int kBM = 128, kBN = 128;
+template <bool A_KM, bool B_NK, class Epi>
+hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K, int splits,
+                      int k_chunk, const Epi& epi) {
+  return launch_gemm<kTileM, kTileN, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
+}
 
 // --------------------------------------------------------------------------
 // Split-K reduction of the change followed by the momentum update.
@@ -598,7 +641,7 @@ __global__ __launch_bounds__(kRed) void sse_reduce_kernel(const double* __restri
 // K-splits for a product with few output tiles: enough blocks for two per
 // CU (512), each split at least 256 deep in K.
 int choose_splits(int M, int N, int K) {
-  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  const int tiles = tile_count(M, N);
   if (K < 1024 || tiles >= 512) return 1;
   int s = (512 + tiles - 1) / tiles;
   const int max_s = K / 256;
@@ -610,7 +653,7 @@ int choose_output_splits(int M, int N, int K) { return choose_splits(M, N, K); }
 
 int chunk_for(int K, int splits) {
   int c = (K + splits - 1) / splits;
-  return (c + BK - 1) / BK * BK;
+  return (c + kChunkAlign - 1) / kChunkAlign * kChunkAlign;
 }
 
 }  // namespace
@@ -623,11 +666,11 @@ LaunchEvents& launch_events() {
   return ev;
 }
 
-int colsum_rows(int M) { return (M + kBM - 1) / kBM; }
+int colsum_rows(int M) { return (M + 127) / 128; }
 
 int output_delta_blocks(int M, int N, int K) {
   if (choose_output_splits(M, N, K) > 1) return ((M + 127) / 128) * ((N + 63) / 64);
-  return ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  return tile_count(M, N);
 }
 
 size_t output_delta_workspace(int M, int N, int K) {
@@ -641,7 +684,7 @@ int output_delta_splits(int M, int N, int K) { return choose_output_splits(M, N,
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
                          const float* bias, float* out, int ldo) {
   EpiSigmoid e{bias, out, ldo};
-  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+  return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
 }
 
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
@@ -650,11 +693,11 @@ hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const fl
   const int sp = choose_output_splits(M, N, K);
   if (sp <= 1) {
     EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs};
-    return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+    return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
   EpiPartial e{ws, ldp, (size_t)M * ldp};
-  return launch_gemm<kBM, kBN, false, false>(s, A, lda, W, ldw, M, N, K, sp, chunk_for(K, sp), e);
+  return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, sp, chunk_for(K, sp), e);
 }
 
 hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
@@ -670,7 +713,7 @@ hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, 
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,
                           const float* act, int lda, float* out, int ldo, float* colsum, int ldcs) {
   EpiHiddenDelta e{act, lda, out, ldo, colsum, ldcs};
-  return launch_gemm<kBM, kBN, false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
+  return launch_cfg<false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 
 int change_splits(int M, int N, int K) { return choose_splits(M, N, K); }
@@ -688,11 +731,11 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
   const int sp = choose_splits(M, N, K);
   if (sp <= 1) {
     EpiUpdate e{W, V, ldw, lr, mom};
-    return launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
+    return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
   EpiPartial e{ws, ldp, (size_t)M * ldp};
-  return launch_gemm<kBM, kBN, true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
+  return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
 }
 
 hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
