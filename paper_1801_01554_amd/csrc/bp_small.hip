@@ -30,41 +30,18 @@ constexpr int kT = 256;        // threads per forward/backward block
 constexpr int kTU = 1024;      // threads per update block (16 waves)
 constexpr int kWU = kTU / 64;
 constexpr int kMaxP = 8;       // patterns per forward/backward block
-constexpr int kU = 32;         // loads kept in flight per lane in the batch sums
+constexpr int kStageFloats = 32768;   // LDS floats the update blocks stage batch chunks in
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
 
-// sum_{p in [r0, r1)} x[p * ldx] * y[p * ldy], added in pattern order; the
-// loads of kU consecutive patterns are issued before their products are added.
-__device__ __forceinline__ float dot_rows(const float* __restrict__ x, int ldx, const float* __restrict__ y, int ldy,
-                                          int r0, int r1) {
-  float g = 0.f;
-  for (int p = r0; p < r1; p += kU) {
-    float a[kU], d[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      a[u] = p + u < r1 ? x[(size_t)(p + u) * ldx] : 0.f;
-      d[u] = p + u < r1 ? y[(size_t)(p + u) * ldy] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      if (p + u < r1) g += a[u] * d[u];
-  }
-  return g;
-}
-
-// sum_{p in [r0, r1)} y[p * ldy], added in pattern order, kU loads in flight.
-__device__ __forceinline__ float sum_rows(const float* __restrict__ y, int ldy, int r0, int r1) {
-  float g = 0.f;
-  for (int p = r0; p < r1; p += kU) {
-    float d[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) d[u] = p + u < r1 ? y[(size_t)(p + u) * ldy] : 0.f;
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      if (p + u < r1) g += d[u];
-  }
-  return g;
+// q / d and q % d for 0 <= q < 2^16 and 1 <= d <= 2^10, through a float
+// reciprocal: the float quotient is within 2^-8 / d of the true one, far from
+// the next integer, so the truncation is exact.
+__device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int& rem) {
+  quo = (int)(((float)q + 0.5f) * inv_d);
+  rem = q - quo * d;
 }
 
 // Dynamic LDS of small_fwdbwd: W1 as (H + 1) x (O + 1) (odd row stride so
@@ -91,24 +68,28 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   const int tid = threadIdx.x;
   const int p0 = blockIdx.x * P;
   const int np = min(P, rows - p0);
+  const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
   // round 1 (np * n_active <= kT and np * O <= 2 kT by the path's limits)
   {
-    const int ni = np * n_active, nt = np * O, nw1 = (H + 1) * O;
+    const int ni = np * n_active, nt = np * O;
     const int iv = tid < ni ? act[(size_t)p0 * n_active + tid] : 0;       // rows of act are contiguous
     const float t0 = tid < nt ? T[(size_t)p0 * O + tid] : 0.f;            // rows of T are contiguous
     const float t1 = tid + kT < nt ? T[(size_t)p0 * O + tid + kT] : 0.f;
-    for (int q0 = 0; q0 < nw1; q0 += 16 * kT) {
+    // W1: lane column c = tid % cw, rows tid / cw + k (kT / cw)
+    const int cw = O <= 32 ? 32 : 64, rpp = kT / cw;
+    const int c = tid & (cw - 1), jt = tid / cw;
+    for (int k0 = 0; k0 * rpp <= H; k0 += 16) {
       float v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int q = q0 + u * kT + tid;
-        v[u] = q < nw1 ? W1[(size_t)(q / O) * ldw1 + q % O] : 0.f;
+        const int j = jt + (k0 + u) * rpp;
+        v[u] = (c < O && j <= H) ? W1[(size_t)j * ldw1 + c] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
-        const int q = q0 + u * kT + tid;
-        if (q < nw1) w1s[(q / O) * S1 + q % O] = v[u];
+        const int j = jt + (k0 + u) * rpp;
+        if (c < O && j <= H) w1s[j * S1 + c] = v[u];
       }
     }
     if (tid < ni) idx[tid] = iv;
@@ -146,16 +127,18 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   float sse = 0.f;
   {
     const int nout = np * O;
-    int lpo = 8;
-    while (lpo > 1 && nout * lpo > kT) lpo >>= 1;
-    for (int t0 = 0; t0 < nout * lpo; t0 += kT) {
+    int lg = 3;
+    while (lg > 0 && (nout << lg) > kT) --lg;
+    const int lpo = 1 << lg;
+    for (int t0 = 0; t0 < (nout << lg); t0 += kT) {
       const int t = t0 + tid;
-      const int q = t / lpo, part = t % lpo;
+      const int q = t >> lg, part = t & (lpo - 1);
+      int p = 0, c = 0;
+      divmod(q, O, inv_O, p, c);
       float z = 0.f;
       if (q < nout) {
-        const int p = q / O, c = q % O;
         const float* h = hs + p * H;
-        const int j0 = H * part / lpo, j1 = H * (part + 1) / lpo;
+        const int j0 = (H * part) >> lg, j1 = (H * (part + 1)) >> lg;
         for (int j = j0; j < j1; j += 8) {
           float hv[8], wv[8];
 #pragma unroll
@@ -169,7 +152,6 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       }
       for (int m = 1; m < lpo; m <<= 1) z += __shfl_xor(z, m, 64);
       if (q < nout && part == 0) {
-        const int p = q / O, c = q % O;
         const float y = logistic(w1s[H * S1 + c] + z);
         const float e = ts[q] - y;
         sse += e * e;
@@ -182,7 +164,8 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   __syncthreads();
   // hidden deltas (W1 before its update, bias row excluded): one thread per (p, j)
   for (int t = tid; t < np * H; t += kT) {
-    const int p = t / H, j = t % H;
+    int p, j;
+    divmod(t, H, inv_H, p, j);
     const float* wr = w1s + j * S1;
     const float* d = d2s + p * O;
     float s = 0.f;
@@ -211,44 +194,41 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   }
 }
 
-// Sum of the kWU wave partials of one lane, in wave order.
-__device__ __forceinline__ float combine(const float (*part)[64], int lane) {
-  float s = part[0][lane];
-  for (int w = 1; w < kWU; ++w) s += part[w][lane];
-  return s;
-}
-
 // 1024 threads = 16 waves per block.  The weight and momentum a lane updates
-// are loaded at the start, overlapping the batch sums.
-// Blocks [0, nA): W1 changes, 64 consecutive elements (j, c) per block, the
-//   16 waves summing consecutive sixteenths of the batch.
+// are loaded at the start, overlapping the sums.  Batch sums over patterns
+// run in chunks of `ch` patterns staged in LDS with wide coalesced loads; wave
+// w adds its sixteenth of each chunk in pattern order, and the 16 wave
+// partials are combined in wave order.
+// Blocks [0, nA): W1 elements o = 64 b + lane (row o / O, column o % O):
+//   sum_p A1[p][j] D2[p][c] (the bias row H takes 1 for A1).
 // Blocks [nA, nA + n0): row r of W0: the delta rows of the patterns whose
-//   active list contains r, in pattern order (ballot compaction of 1024
+//   active list holds r, in pattern order (ballot compaction of 1024
 //   patterns at a time); wave w owns the column strip (w % 4) and quarter
 //   (w / 4) of each compacted list.
-// Blocks [nA + n0, nA + n0 + nS): the bias row of W0, 64 columns per block,
-//   the 16 waves summing consecutive sixteenths of the batch.
+// Blocks [nA + n0, nA + n0 + nS): the bias row of W0, 64 columns per block:
+//   sum_p D1[p][j].
 __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                            const float* __restrict__ A1, const float* __restrict__ D1,
                                                            int lda1, const float* __restrict__ D2, int ldd2,
                                                            float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                                                           float* V1, int ldw1, int O, int nA, float lr, float mom) {
+                                                           float* V1, int ldw1, int O, int nA, int ch, float lr,
+                                                           float mom) {
+  extern __shared__ float stage[];
   __shared__ float part[kWU][64];
   __shared__ int list[kTU];
   __shared__ int wave_cnt[kWU];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
-  const int r0 = (int)((int64_t)rows * wave / kWU), r1 = (int)((int64_t)rows * (wave + 1) / kWU);
 
   float* Wt;        // weight row this block updates
   float* Vt;
   int col, ncol;    // lane's column in that row, row length
+  int jrow = 0;     // W1 blocks: the lane's row
   if (b < nA) {
     const int o = b * 64 + lane;
-    const int j = o / O, c = o % O;
-    Wt = W1 + (size_t)j * ldw1;
-    Vt = V1 + (size_t)j * ldw1;
-    col = c;
+    divmod(o, O, 1.0f / (float)O, jrow, col);
+    Wt = W1 + (size_t)jrow * ldw1;
+    Vt = V1 + (size_t)jrow * ldw1;
     ncol = o < (H + 1) * O ? O : 0;
   } else if (b < nA + n0) {
     Wt = W0 + (size_t)(b - nA) * ldw0;
@@ -271,12 +251,60 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
 
   float g = 0.f;
   if (b < nA) {
-    const int o = b * 64 + lane;
-    const int j = o / O, c = o % O;
-    if (live) g = (j < H) ? dot_rows(A1 + j, lda1, D2 + c, ldd2, r0, r1) : sum_rows(D2 + c, ldd2, r0, r1);
+    // rows jlo .. jhi of W1 are touched by this block
+    const int jlo = (b * 64) / O, jhi = min(H, (b * 64 + 63) / O), nj = jhi - jlo + 1;
+    const float inv_nj = 1.0f / (float)nj;
+    const int q4 = ldd2 >> 2;                       // float4 per D2 row (ldd2 % 4 == 0)
+    float* d2s = stage;                             // [ch][ldd2]
+    float* a1s = stage + ch * ldd2;                 // [ch][nj]
+    for (int pc = 0; pc < rows; pc += ch) {
+      const int cn = min(ch, rows - pc);
+      const f32x4* src = reinterpret_cast<const f32x4*>(D2 + (size_t)pc * ldd2);
+      for (int i0 = tid; i0 < cn * q4; i0 += 4 * kTU) {
+        f32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kTU < cn * q4 ? src[i0 + u * kTU] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kTU < cn * q4) reinterpret_cast<f32x4*>(d2s)[i0 + u * kTU] = v[u];
+      }
+      for (int i0 = tid; i0 < cn * nj; i0 += 4 * kTU) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int i = i0 + u * kTU;
+          int p = 0, jj = 0;
+          divmod(i, nj, inv_nj, p, jj);
+          v[u] = (i < cn * nj && jlo + jj < H) ? A1[(size_t)(pc + p) * lda1 + jlo + jj] : 1.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kTU < cn * nj) a1s[i0 + u * kTU] = v[u];
+      }
+      __syncthreads();
+      const int s0 = cn * wave / kWU, s1 = cn * (wave + 1) / kWU;
+      if (live) {
+        const int jj = jrow - jlo;
+        for (int p = s0; p < s1; p += 8) {
+          float av[8], dv[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            av[u] = p + u < s1 ? a1s[(p + u) * nj + jj] : 0.f;
+            dv[u] = p + u < s1 ? d2s[(p + u) * ldd2 + col] : 0.f;
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (p + u < s1) g += av[u] * dv[u];
+        }
+      }
+      __syncthreads();
+    }
     part[wave][lane] = g;
     __syncthreads();
-    if (owner) g = combine(part, lane);
+    if (owner) {
+      g = part[0][lane];
+      for (int w = 1; w < kWU; ++w) g += part[w][lane];
+    }
   } else if (b < nA + n0) {
     const int r = b - nA;
     const int quarter = wave >> 2;
@@ -285,10 +313,10 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       bool hit = false;
       if (p < rows) {
         const int32_t* a = act + (size_t)p * n_active;
-        for (int k0 = 0; k0 < n_active; k0 += 8) {
+        for (int q0 = 0; q0 < n_active; q0 += 8) {
           int iv[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) iv[u] = k0 + u < n_active ? a[k0 + u] : -1;
+          for (int u = 0; u < 8; ++u) iv[u] = q0 + u < n_active ? a[q0 + u] : -1;
 #pragma unroll
           for (int u = 0; u < 8; ++u) hit |= (iv[u] == r);
         }
@@ -322,10 +350,46 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       __syncthreads();
     }
   } else {
-    if (live) g = sum_rows(D1 + col, lda1, r0, r1);
+    // bias row of W0: columns c0 .. c0 + 63 of D1, staged as float4 (a D1
+    // row is lda1 floats, lda1 % 4 == 0; lanes past H are never summed)
+    const int c0 = (b - nA - n0) * 64;
+    float* d1s = stage;                             // [ch][64]
+    for (int pc = 0; pc < rows; pc += ch) {
+      const int cn = min(ch, rows - pc);
+      for (int i0 = tid; i0 < cn * 16; i0 += 8 * kTU) {
+        f32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * kTU;
+          const int cc = c0 + (i & 15) * 4;
+          v[u] = (i < cn * 16 && cc < lda1)
+                     ? *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 4)) * lda1 + cc)
+                     : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (i0 + u * kTU < cn * 16) reinterpret_cast<f32x4*>(d1s)[i0 + u * kTU] = v[u];
+      }
+      __syncthreads();
+      const int s0 = cn * wave / kWU, s1 = cn * (wave + 1) / kWU;
+      if (live) {
+        for (int p = s0; p < s1; p += 8) {
+          float dv[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) dv[u] = p + u < s1 ? d1s[(p + u) * 64 + lane] : 0.f;
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (p + u < s1) g += dv[u];
+        }
+      }
+      __syncthreads();
+    }
     part[wave][lane] = g;
     __syncthreads();
-    if (owner) g = combine(part, lane);
+    if (owner) {
+      g = part[0][lane];
+      for (int w = 1; w < kWU; ++w) g += part[w][lane];
+    }
   }
   if (owner && live) {
     const float v = lr * g + mom * v_old;
@@ -368,8 +432,15 @@ hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int row
   if (rows <= 0) return hipSuccess;
   const int nA = ((H + 1) * O + 63) / 64;
   const int nS = (H + 63) / 64;
-  return launch_kernel(small_update_kernel, nA + n0 + nS, kTU, 0, s, act, n_active, rows, A1, D1, lda1, D2, ldd2, W0, V0, ldw0, n0, H, W1,
-                                                  V1, ldw1, O, nA, lr, mom);
+  // patterns staged per round: the largest power of two that fits
+  // kStageFloats for both block types (>= 128 since ldd2 + njmax <= 134)
+  const int njmax = 64 / O + 2;
+  const int per = (ldd2 + njmax) > 64 ? (ldd2 + njmax) : 64;
+  int ch = 1;
+  while (ch * 2 * per <= kStageFloats) ch *= 2;
+  const size_t lds = sizeof(float) * (size_t)ch * per;
+  return launch_kernel(small_update_kernel, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2, ldd2,
+                       W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom);
 }
 
 }  // namespace bpk
