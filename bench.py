@@ -212,21 +212,122 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
     return res, w
 
 
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_BYTES = 1 << 30        # one copy of 1 GiB for the counter calibration
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for f in ("bp_kernels.hip", "bp_small.hip"):
+        h.update(open(os.path.join(ROOT, "paper_1801_01554_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def traffic_for(workload, kind):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it matches the current kernels."""
-    p = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(p):
+    if not os.path.exists(TRAFFIC_JSON):
         return None
     try:
-        with open(p) as f:
+        with open(TRAFFIC_JSON) as f:
             d = json.load(f)
-        src = os.path.join(ROOT, "paper_1801_01554_amd", "csrc", "bp_kernels.hip")
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if d.get("kernel_source_sha256") != sha:
+        if d.get("kernel_source_sha256") != kernel_source_sha():
             return None
-        return d.get("workloads", {}).get(workload, {}).get(kind)
-    except (OSError, ValueError):
+        e = d.get("workloads", {}).get(workload, {}).get(kind)
+        return e["hbm_bytes_per_launch"] if e else None
+    except (OSError, ValueError, KeyError):
         return None
+
+
+def kind_of_kernel(name):
+    """Kernel kind of a rocprofv3 kernel name."""
+    import re
+    m = re.search(r"gemm_kernel<\d+, \d+, \d+, (true|false), (true|false), (true|false), (true|false), [^>]*?(\w+)>", name)
+    if m:
+        epi = m.group(5)
+        if epi == "EpiPartial":
+            return "change" if m.group(1) == "true" else "output"
+        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
+                "EpiUpdate": "change"}.get(epi)
+    for k, v in KERNEL_NAMES.items():
+        if "<" not in v and v in name:
+            return k
+    return None
+
+
+def summarize_stats(src, out, title, note, cmd):
+    """Writes a rocprofv3 --stats kernel_stats.csv as the markdown summary kept in profiles/."""
+    import csv
+    import re
+    lines = [f"# {title}", "", note, "", "Command (on the MI355X box, from /tmp with TMPDIR=/tmp; R = repository root):",
+             "", f"    {cmd}", "", "| kernel | calls | total ns | average ns | % | min ns | max ns |",
+             "|---|---|---|---|---|---|---|"]
+    for r in csv.DictReader(open(src)):
+        name = r["Name"].replace("bpk::(anonymous namespace)::", "")
+        m = re.search(r"(gemm_kernel<[^>]*>|\w+_kernel|fillBufferAligned)", name)
+        short = m.group(1) if m else name[:60]
+        lines.append(f"| `{short}` | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | "
+                     f"{float(r['Percentage']):.1f} | {r['MinNs']} | {r['MaxNs']} |")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def copy_calibration():
+    """Copies a 1 GiB buffer four times (device to device), for the FETCH_SIZE / WRITE_SIZE scale."""
+    import torch
+    x = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    y = torch.empty_like(x)
+    for _ in range(4):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(f"copied {COPY_BYTES} bytes x 4", flush=True)
+
+
+def counters_to_traffic(workload, fetch_csv, write_csv, calib_fetch_csv, calib_write_csv, command):
+    """Turns rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE passes into per-launch HBM bytes in profiles/traffic.json."""
+    import csv
+    import collections
+
+    def per_kernel(path, counter):
+        acc = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return acc
+
+    def copy_factor(path, counter):
+        acc = per_kernel(path, counter)
+        # the copy is the dispatch with the largest counter value
+        name, vals = max(acc.items(), key=lambda kv: max(kv[1]))
+        return COPY_BYTES / (max(vals) * 1024.0), name
+
+    ff, fname = copy_factor(calib_fetch_csv, "FETCH_SIZE")
+    wf, _ = copy_factor(calib_write_csv, "WRITE_SIZE")
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    kinds = collections.defaultdict(lambda: [0.0, 0.0, 0])
+    for name, vals in fetch.items():
+        k = kind_of_kernel(name)
+        if k:
+            kinds[k][0] += sum(vals) * 1024.0 * ff
+            kinds[k][2] += len(vals)
+    for name, vals in write.items():
+        k = kind_of_kernel(name)
+        if k:
+            kinds[k][1] += sum(vals) * 1024.0 * wf
+    d = {}
+    if os.path.exists(TRAFFIC_JSON):
+        d = json.load(open(TRAFFIC_JSON))
+    sha = kernel_source_sha()
+    if d.get("kernel_source_sha256") != sha:
+        d = {"kernel_source_sha256": sha, "workloads": {}}
+    d["calibration"] = {"copy_bytes": COPY_BYTES, "copy_kernel": fname, "fetch_factor": ff, "write_factor": wf}
+    d["workloads"][workload] = {
+        k: {"dispatches": n, "fetch_bytes_per_launch": fb / n, "write_bytes_per_launch": wb / n,
+            "hbm_bytes_per_launch": (fb + wb) / n} for k, (fb, wb, n) in kinds.items() if n}
+    d.setdefault("commands", {})[workload] = command
+    with open(TRAFFIC_JSON, "w") as f:
+        json.dump(d, f, indent=1)
+    print(json.dumps(d["workloads"][workload], indent=1))
 
 
 def cpu_baseline(w, budget_s, log):
@@ -277,7 +378,22 @@ def main():
     ap.add_argument("--no-secondary", action="store_true", help="skip the wide and deep dense nets")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for the baseline")
+    ap.add_argument("--copy-calibration", action="store_true", help="only copy 1 GiB four times (counter scale)")
+    ap.add_argument("--counters-to-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH", "CAL_WRITE"),
+                    help="write per-launch HBM traffic of --workload to profiles/traffic.json")
+    ap.add_argument("--command", default="", help="the profiling command recorded with --counters-to-traffic")
+    ap.add_argument("--summarize-stats", nargs=5, metavar=("STATS_CSV", "OUT_MD", "TITLE", "NOTE", "CMD"),
+                    help="format a rocprofv3 kernel_stats.csv as a profiles/ summary")
     args = ap.parse_args()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
+    if args.counters_to_traffic:
+        counters_to_traffic(args.workload, *args.counters_to_traffic, args.command)
+        return
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the design notes describe how the "
