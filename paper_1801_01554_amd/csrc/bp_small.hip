@@ -51,8 +51,12 @@ __device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int&
 //
 // The kernel has two rounds of global loads: (1) indices, targets and W1,
 // all independent; (2) the gathered W0 rows of all the block's patterns.
+// P (patterns per block) is a template parameter so that each instantiation
+// holds only the unrolled code it runs: these kernels are short enough that
+// instruction-cache misses at launch are a visible part of their time.
+template <int P>
 __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restrict__ act, int n_active, int rows,
-                                                          int P, const float* __restrict__ W0, int ldw0, int n0,
+                                                          const float* __restrict__ W0, int ldw0, int n0,
                                                           int H, const float* __restrict__ W1, int ldw1, int O,
                                                           const float* __restrict__ T, float* A1, int lda1,
                                                           float* D1, float* D2, int ldd2, double* sse_part) {
@@ -73,9 +77,12 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   // round 1 (np * n_active <= kT and np * O <= 2 kT by the path's limits)
   {
     const int ni = np * n_active, nt = np * O;
-    const int iv = tid < ni ? act[(size_t)p0 * n_active + tid] : 0;       // rows of act are contiguous
-    const float t0 = tid < nt ? T[(size_t)p0 * O + tid] : 0.f;            // rows of T are contiguous
-    const float t1 = tid + kT < nt ? T[(size_t)p0 * O + tid + kT] : 0.f;
+    // Every load below reads a clamped, valid address and the predicate only
+    // selects the value: no load sits behind a branch, so all are in flight
+    // together.  (Rows of act and of T are contiguous.)
+    const int iv = act[(size_t)p0 * n_active + min(tid, ni - 1)];
+    const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
+    const float t1 = T[(size_t)p0 * O + min(tid + kT, nt - 1)];
     // W1: lane column c = tid % cw, rows tid / cw + k (kT / cw)
     const int cw = O <= 32 ? 32 : 64, rpp = kT / cw;
     const int c = tid & (cw - 1), jt = tid / cw;
@@ -84,7 +91,7 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int j = jt + (k0 + u) * rpp;
-        v[u] = (c < O && j <= H) ? W1[(size_t)j * ldw1 + c] : 0.f;
+        v[u] = W1[(size_t)min(j, H) * ldw1 + min(c, O - 1)];
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
@@ -100,14 +107,14 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   // round 2: hidden layer, net = bias + sum of the active rows of W0 (in index order)
   for (int j = tid; j < H; j += kT) {
     const float b = W0[(size_t)n0 * ldw0 + j];
-    float v[kMaxP][8];
+    float v[P][8];
 #pragma unroll
-    for (int p = 0; p < kMaxP; ++p)
+    for (int p = 0; p < P; ++p)
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        v[p][u] = (p < np && u < n_active) ? W0[(size_t)idx[p * n_active + u] * ldw0 + j] : 0.f;
+        v[p][u] = W0[(size_t)idx[min(p, np - 1) * n_active + min(u, n_active - 1)] * ldw0 + j];
 #pragma unroll
-    for (int p = 0; p < kMaxP; ++p) {
+    for (int p = 0; p < P; ++p) {
       if (p >= np) break;
       float net = b;
 #pragma unroll
@@ -143,8 +150,9 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
           float hv[8], wv[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
-            hv[u] = j + u < j1 ? h[j + u] : 0.f;
-            wv[u] = j + u < j1 ? w1s[(j + u) * S1 + c] : 0.f;
+            const int jc = min(j + u, j1 - 1);
+            hv[u] = j + u < j1 ? h[jc] : 0.f;
+            wv[u] = w1s[jc * S1 + c];
           }
 #pragma unroll
           for (int u = 0; u < 8; ++u) z += hv[u] * wv[u];
@@ -173,8 +181,9 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       float wv[8], dv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        wv[u] = c + u < O ? wr[c + u] : 0.f;
-        dv[u] = c + u < O ? d[c + u] : 0.f;
+        const int cc = min(c + u, O - 1);
+        wv[u] = wr[cc];
+        dv[u] = c + u < O ? d[cc] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) s += wv[u] * dv[u];
@@ -263,7 +272,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       for (int i0 = tid; i0 < cn * q4; i0 += 4 * kTU) {
         f32x4 v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kTU < cn * q4 ? src[i0 + u * kTU] : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < 4; ++u) v[u] = src[min(i0 + u * kTU, cn * q4 - 1)];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
           if (i0 + u * kTU < cn * q4) reinterpret_cast<f32x4*>(d2s)[i0 + u * kTU] = v[u];
@@ -272,10 +281,11 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         float v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int i = i0 + u * kTU;
+          const int i = min(i0 + u * kTU, cn * nj - 1);
           int p = 0, jj = 0;
           divmod(i, nj, inv_nj, p, jj);
-          v[u] = (i < cn * nj && jlo + jj < H) ? A1[(size_t)(pc + p) * lda1 + jlo + jj] : 1.f;
+          const float a = A1[(size_t)(pc + p) * lda1 + min(jlo + jj, H - 1)];
+          v[u] = jlo + jj < H ? a : 1.f;
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
@@ -289,8 +299,9 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
           float av[8], dv[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
-            av[u] = p + u < s1 ? a1s[(p + u) * nj + jj] : 0.f;
-            dv[u] = p + u < s1 ? d2s[(p + u) * ldd2 + col] : 0.f;
+            const int pp = min(p + u, s1 - 1);
+            av[u] = a1s[pp * nj + jj];
+            dv[u] = d2s[pp * ldd2 + col];
           }
 #pragma unroll
           for (int u = 0; u < 8; ++u)
@@ -316,7 +327,9 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         for (int q0 = 0; q0 < n_active; q0 += 8) {
           int iv[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) iv[u] = q0 + u < n_active ? a[q0 + u] : -1;
+          for (int u = 0; u < 8; ++u) iv[u] = a[min(q0 + u, n_active - 1)];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) iv[u] = q0 + u < n_active ? iv[u] : -1;
 #pragma unroll
           for (int u = 0; u < 8; ++u) hit |= (iv[u] == r);
         }
@@ -337,7 +350,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         for (int q = q0; q < q1; q += 16) {
           float v[16];
 #pragma unroll
-          for (int u = 0; u < 16; ++u) v[u] = q + u < q1 ? D1[(size_t)list[q + u] * lda1 + col] : 0.f;
+          for (int u = 0; u < 16; ++u) v[u] = D1[(size_t)list[min(q + u, q1 - 1)] * lda1 + col];
 #pragma unroll
           for (int u = 0; u < 16; ++u)
             if (q + u < q1) s += v[u];
@@ -360,11 +373,9 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         f32x4 v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const int i = i0 + u * kTU;
-          const int cc = c0 + (i & 15) * 4;
-          v[u] = (i < cn * 16 && cc < lda1)
-                     ? *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 4)) * lda1 + cc)
-                     : f32x4{0.f, 0.f, 0.f, 0.f};
+          const int i = min(i0 + u * kTU, cn * 16 - 1);
+          const int cc = min(c0 + (i & 15) * 4, lda1 - 4);
+          v[u] = *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 4)) * lda1 + cc);
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u)
@@ -376,7 +387,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         for (int p = s0; p < s1; p += 8) {
           float dv[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) dv[u] = p + u < s1 ? d1s[(p + u) * 64 + lane] : 0.f;
+          for (int u = 0; u < 8; ++u) dv[u] = d1s[min(p + u, s1 - 1) * 64 + lane];
 #pragma unroll
           for (int u = 0; u < 8; ++u)
             if (p + u < s1) g += dv[u];
@@ -398,9 +409,11 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
   }
 }
 
+// Patterns per forward/backward block: a power of two, about rows / 256.
 int patterns_per_block(int rows) {
-  int p = rows / 256;
-  return p < 1 ? 1 : (p > kMaxP ? kMaxP : p);
+  int p = 1;
+  while (p < kMaxP && 2 * p * 256 <= rows) p *= 2;
+  return p;
 }
 
 }  // namespace
@@ -422,8 +435,13 @@ hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int row
   const int P = patterns_per_block(rows);
   const size_t lds = sizeof(float) * ((size_t)(H + 1) * (O + 1) + (size_t)P * H + 2 * (size_t)P * O) +
                      sizeof(int) * (size_t)P * n_active;
-  return launch_kernel(small_fwdbwd_kernel, small_fwdbwd_blocks(rows), kT, lds, s, act, n_active, rows, P, W0, ldw0, n0, H, W1, ldw1, O,
-                                                                 T, A1, lda1, D1, D2, ldd2, sse_part);
+  const int nb = small_fwdbwd_blocks(rows);
+  switch (P) {
+    case 1: return launch_kernel(small_fwdbwd_kernel<1>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
+    case 2: return launch_kernel(small_fwdbwd_kernel<2>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
+    case 4: return launch_kernel(small_fwdbwd_kernel<4>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
+    default: return launch_kernel(small_fwdbwd_kernel<8>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
+  }
 }
 
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
