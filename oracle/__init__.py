@@ -53,6 +53,14 @@ def load():
         "orc_train_epoch_onehot": (ctypes.c_int, [vp, _i32p, ctypes.c_int32, _f32p, ctypes.c_int64,
                                                   ctypes.c_int32, ctypes.c_double, ctypes.c_double,
                                                   _f64p, _f64p]),
+        "orc_set_sigmoid": (ctypes.c_int, [vp, ctypes.c_int32]),
+        "orc_eval_sigmoid": (ctypes.c_int, [vp, _f64p, ctypes.c_int64, _f64p]),
+        "orc_set_fault_limit": (ctypes.c_int, [vp, ctypes.c_double]),
+        "orc_fault_count": (ctypes.c_int64, [vp]),
+        "orc_checkpoint_save": (ctypes.c_int, [vp]),
+        "orc_checkpoint_restore": (ctypes.c_int, [vp]),
+        "orc_guard_config": (ctypes.c_int, [vp, ctypes.c_int32, ctypes.c_double]),
+        "orc_guard_epoch": (ctypes.c_int, [vp, ctypes.c_double]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -144,6 +152,44 @@ class OracleNet:
             out.append(flat[o:o + r * c].reshape(r, c))
             o += r * c
         return out
+
+    # options -------------------------------------------------------------
+    SIGMOID_EXACT, SIGMOID_TABLE = 0, 1
+
+    def set_sigmoid(self, mode: int) -> None:
+        """0: exact logistic; 1: the 256-entry interpolated table on [-15, 15] (section 4.3)."""
+        self._chk(_lib.orc_set_sigmoid(self._h, int(mode)), "set_sigmoid")
+
+    def eval_sigmoid(self, z) -> np.ndarray:
+        """The net's unit nonlinearity at each z (rounded to the storage precision)."""
+        z = np.ascontiguousarray(z, dtype=np.float64).reshape(-1)
+        y = np.empty_like(z)
+        self._chk(_lib.orc_eval_sigmoid(self._h, _p(z, _f64p), z.size, _p(y, _f64p)), "eval_sigmoid")
+        return y
+
+    def set_fault_limit(self, limit: float) -> None:
+        """Range check of the summed changes (section 8): limit > 0 enables, 0 disables; resets the count."""
+        self._chk(_lib.orc_set_fault_limit(self._h, float(limit)), "set_fault_limit")
+
+    def fault_count(self) -> int:
+        return int(_lib.orc_fault_count(self._h))
+
+    def checkpoint_save(self) -> None:
+        self._chk(_lib.orc_checkpoint_save(self._h), "checkpoint_save")
+
+    def checkpoint_restore(self) -> None:
+        self._chk(_lib.orc_checkpoint_restore(self._h), "checkpoint_restore")
+
+    def guard_config(self, every: int, jump: float) -> None:
+        """Checkpoint now and every `every` accepted epochs; roll back when an epoch's error > jump x the last."""
+        self._chk(_lib.orc_guard_config(self._h, int(every), float(jump)), "guard_config")
+
+    def guard_epoch(self, sse: float) -> int:
+        """Reports an epoch's error; returns 1 if the net was rolled back to its checkpoint, else 0."""
+        rc = int(_lib.orc_guard_epoch(self._h, float(sse)))
+        if rc < 0:
+            raise OracleError("guard_epoch: guard not configured")
+        return rc
 
     # method --------------------------------------------------------------
     def forward(self, x=None, active=None) -> np.ndarray:

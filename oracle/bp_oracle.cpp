@@ -46,6 +46,26 @@
  * is the plain definition; the float instance rounds at the storage points a
  * float32 implementation has, which measures the float32 noise floor.
  *
+ * Options (off by default):
+ *   table sigmoid   the second of the two sigmoid evaluations of section 4.3:
+ *             inputs outside [-15, 15] are taken to the ends of that range, the
+ *             range is mapped onto [0, 255] by an add and a multiply, the
+ *             integer part of the result indexes a 256-entry table of the
+ *             logistic at equally spaced points of [-15, 15], and the
+ *             fractional part interpolates linearly to the next entry.  The
+ *             index (an integer that floating point decides) is computed in
+ *             single precision, the interpolation in double.  Table entries
+ *             are Real.
+ *   range check     each summed change G (the "total weight change" of section
+ *             8) outside [-limit, limit], or not a number, is set to zero
+ *             before the update and counted as a fault (section 8).
+ *   checkpoint      one stored copy of W and V (section 10.4), and a guard that
+ *             saves it every `every` accepted epochs and restores it when an
+ *             epoch's error exceeds `jump` times the last accepted epoch's
+ *             error.  A jump that recurs at the same epoch after a rollback is
+ *             accepted: the training is deterministic, so a recurring jump is
+ *             the learning itself, not a transient fault.
+ *
  * Parallelism (OpenMP) only splits independent work: patterns in the forward
  * and backward passes, and output rows in the batch sum, where every element
  * is still accumulated over the patterns in pattern order.  Results do not
@@ -62,6 +82,24 @@
 
 namespace {
 
+double sigmoid(double z) { return 1.0 / (1.0 + std::exp(-z)); }
+
+constexpr int kTableSize = 256;     // entries of the sigmoid table (section 4.3, figure 3)
+constexpr double kTableEnd = 15.0;  // the table covers [-15, 15]
+
+// Checkpoint guard state (see the header comment).
+struct Guard {
+  bool on = false;
+  int every = 1;
+  double jump = 0.0;
+  int since = 0;            // epochs accepted since the checkpoint
+  int retry_at = -1;        // epoch (counted from the checkpoint) that was already rolled back
+  bool have_last = false;
+  double last_sse = 0.0;    // error of the last accepted epoch
+  bool ck_have = false;
+  double ck_sse = 0.0;      // error of the epoch at which the checkpoint was taken
+};
+
 template <typename Real>
 struct Net {
   int L = 0;                    // number of weight layers
@@ -69,13 +107,40 @@ struct Net {
   std::vector<int64_t> off;     // offset of W_l in the flat arrays
   int64_t total = 0;            // sum (n_l + 1) * n_{l+1}
   std::vector<Real> W, V;       // flat, layer l row-major (n_l + 1) x n_{l+1}
+  int sig_mode = 0;             // 0: exact logistic, 1: table
+  std::vector<Real> table;      // sigmoid table, kTableSize entries
+  double fault_limit = 0.0;     // > 0: range check of the summed changes
+  int64_t faults = 0;
+  std::vector<Real> ckW, ckV;   // checkpoint
+  Guard guard;
 
   const Real* w(int l) const { return W.data() + off[l]; }
   Real* w(int l) { return W.data() + off[l]; }
   Real* v(int l) { return V.data() + off[l]; }
+
+  // The unit nonlinearity in use, evaluated on a net input z.
+  double act(double z) const {
+    if (sig_mode == 0) return sigmoid(z);
+    if (std::isnan(z)) return z;
+    float zf = (float)z;
+    if (zf < (float)-kTableEnd) zf = (float)-kTableEnd;
+    if (zf > (float)kTableEnd) zf = (float)kTableEnd;
+    // [-15, 15] -> [0, 255]: add 15, multiply by 255 / 30 = 8.5 (exact in float)
+    const float x1 = (zf + (float)kTableEnd) * (float)((kTableSize - 1) / (2.0 * kTableEnd));
+    const int i = (int)std::floor(x1);
+    if (i >= kTableSize - 1) return (double)table[kTableSize - 1];
+    const double f = (double)x1 - (double)i;
+    return (double)table[i] + f * ((double)table[i + 1] - (double)table[i]);
+  }
 };
 
-double sigmoid(double z) { return 1.0 / (1.0 + std::exp(-z)); }
+// Entry i of the sigmoid table: the logistic at -15 + 30 i / 255.
+template <typename Real>
+void build_table(Net<Real>& net) {
+  net.table.assign(kTableSize, (Real)0);
+  for (int i = 0; i < kTableSize; ++i)
+    net.table[i] = (Real)sigmoid(-kTableEnd + 2.0 * kTableEnd * (double)i / (double)(kTableSize - 1));
+}
 
 // Per-batch state: activations a_0..a_L and deltas delta_1..delta_L of every
 // pattern, stored row by row ([pattern][unit]).
@@ -99,7 +164,7 @@ void forward_pattern(const Net<Real>& net, std::vector<Real*>& a) {
       const Real* row = W + (int64_t)i * n_out;
       for (int j = 0; j < n_out; ++j) acc[j] += ai * (double)row[j];
     }
-    for (int j = 0; j < n_out; ++j) a[l + 1][j] = (Real)sigmoid(acc[j]);
+    for (int j = 0; j < n_out; ++j) a[l + 1][j] = (Real)net.act(acc[j]);
   }
 }
 
@@ -178,12 +243,70 @@ void apply_update(Net<Real>& net, const double* G, double lr, double mom) {
   const int64_t total = net.total;
   Real* W = net.W.data();
   Real* V = net.V.data();
-#pragma omp parallel for schedule(static)
+  const double limit = net.fault_limit;
+  int64_t faults = 0;
+#pragma omp parallel for schedule(static) reduction(+ : faults)
   for (int64_t k = 0; k < total; ++k) {
-    const Real v = (Real)(lr * G[k] + mom * (double)V[k]);
+    double g = G[k];
+    if (limit > 0.0 && !(std::fabs(g) <= limit)) {   // section 8: out of range -> zero, count
+      g = 0.0;
+      ++faults;
+    }
+    const Real v = (Real)(lr * g + mom * (double)V[k]);
     V[k] = v;
     W[k] = (Real)((double)W[k] + (double)v);
   }
+  net.faults += faults;
+}
+
+template <typename Real>
+void save_checkpoint(Net<Real>& net) {
+  net.ckW = net.W;
+  net.ckV = net.V;
+}
+
+template <typename Real>
+int restore_checkpoint(Net<Real>& net) {
+  if (net.ckW.size() != net.W.size()) return -1;
+  net.W = net.ckW;
+  net.V = net.ckV;
+  return 0;
+}
+
+template <typename Real>
+void guard_config(Net<Real>& net, int every, double jump) {
+  net.guard = Guard();
+  net.guard.on = true;
+  net.guard.every = every;
+  net.guard.jump = jump;
+  save_checkpoint(net);
+}
+
+// 0: epoch accepted; 1: rolled back to the checkpoint.
+template <typename Real>
+int guard_epoch(Net<Real>& net, double sse) {
+  Guard& g = net.guard;
+  const int pos = g.since + 1;
+  const bool jumped = g.have_last && !(sse <= g.jump * g.last_sse);
+  if (jumped && g.retry_at != pos) {
+    restore_checkpoint(net);
+    g.retry_at = pos;
+    g.since = 0;
+    g.have_last = g.ck_have;
+    g.last_sse = g.ck_sse;
+    return 1;
+  }
+  g.have_last = true;
+  g.last_sse = sse;
+  g.since = pos;
+  if (g.since == g.every) {
+    save_checkpoint(net);
+    g.ck_have = true;
+    g.ck_sse = sse;
+    g.since = 0;
+    g.retry_at = -1;
+  }
+  return 0;
 }
 
 template <typename Real>
@@ -395,6 +518,67 @@ int orc_get_momentum(const orc_net* h, double* v, int64_t n) {
   if (!h || !v || n != orc_num_weights(h)) return -1;
   for (int64_t k = 0; k < n; ++k) v[k] = h->bits == 32 ? (double)h->f.V[k] : h->d.V[k];
   return 0;
+}
+
+// Sigmoid evaluation: 0 exact logistic, 1 the 256-entry table (section 4.3).
+int orc_set_sigmoid(orc_net* h, int32_t mode) {
+  if (!h || (mode != 0 && mode != 1)) return -1;
+  auto f = [&](auto& net) {
+    net.sig_mode = mode;
+    if (mode == 1) build_table(net);
+    return 0;
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+// The net's unit nonlinearity at each z[k] (for checking it on its own).
+int orc_eval_sigmoid(const orc_net* h, const double* z, int64_t n, double* y) {
+  if (!h || n < 0 || (n > 0 && (!z || !y))) return -1;
+  for (int64_t k = 0; k < n; ++k) y[k] = h->bits == 32 ? (double)(float)h->f.act(z[k]) : h->d.act(z[k]);
+  return 0;
+}
+
+// Range check of the summed changes (section 8): limit > 0 enables, 0 disables; resets the count.
+int orc_set_fault_limit(orc_net* h, double limit) {
+  if (!h || !(limit >= 0.0)) return -1;
+  auto f = [&](auto& net) {
+    net.fault_limit = limit;
+    net.faults = 0;
+    return 0;
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+int64_t orc_fault_count(const orc_net* h) { return !h ? -1 : (h->bits == 32 ? h->f.faults : h->d.faults); }
+
+int orc_checkpoint_save(orc_net* h) {
+  if (!h) return -1;
+  auto f = [&](auto& net) {
+    save_checkpoint(net);
+    return 0;
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_checkpoint_restore(orc_net* h) {
+  if (!h) return -1;
+  auto f = [&](auto& net) { return restore_checkpoint(net); };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_guard_config(orc_net* h, int32_t every, double jump) {
+  if (!h || every < 1 || !(jump > 0.0)) return -1;
+  auto f = [&](auto& net) {
+    guard_config(net, every, jump);
+    return 0;
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_guard_epoch(orc_net* h, double sse) {
+  if (!h) return -1;
+  auto f = [&](auto& net) { return net.guard.on ? guard_epoch(net, sse) : -1; };
+  return ORC_DISPATCH(h, f);
 }
 
 int orc_forward(orc_net* h, const float* x, int64_t n, double* y) {
