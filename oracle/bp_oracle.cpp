@@ -149,11 +149,16 @@ struct BatchState {
   std::vector<std::vector<Real>> a;    // a[l] : rows x n_l
   std::vector<std::vector<Real>> d;    // d[l] : rows x n_l (l >= 1)
   std::vector<double> sse_p;           // squared error of each pattern
+  // One-hot inputs (section 6.3): only the active input units take part in the
+  // first layer, in the forward sum and in the summed change (inactive units
+  // are 0 and contribute nothing; this differs from a dense 0/1 product only
+  // when a weight or a delta is not finite, where 0 * NaN would be NaN).
+  bool sparse0 = false;
 };
 
 // Forward pass of one pattern: a[0] already holds the inputs.
 template <typename Real>
-void forward_pattern(const Net<Real>& net, std::vector<Real*>& a) {
+void forward_pattern(const Net<Real>& net, std::vector<Real*>& a, bool sparse0) {
   for (int l = 0; l < net.L; ++l) {
     const int n_in = net.n[l], n_out = net.n[l + 1];
     const Real* W = net.w(l);
@@ -161,6 +166,7 @@ void forward_pattern(const Net<Real>& net, std::vector<Real*>& a) {
     for (int j = 0; j < n_out; ++j) acc[j] = (double)W[(int64_t)n_in * n_out + j];  // true unit
     for (int i = 0; i < n_in; ++i) {
       const double ai = (double)a[l][i];
+      if (l == 0 && sparse0 && ai == 0.0) continue;
       const Real* row = W + (int64_t)i * n_out;
       for (int j = 0; j < n_out; ++j) acc[j] += ai * (double)row[j];
     }
@@ -202,7 +208,7 @@ void run_batch(const Net<Real>& net, BatchState<Real>& st, int64_t rows, const f
   for (int64_t p = 0; p < rows; ++p) {
     std::vector<Real*> a(L + 1), d(L + 1, nullptr);
     for (int l = 0; l <= L; ++l) a[l] = st.a[l].data() + p * net.n[l];
-    forward_pattern(net, a);
+    forward_pattern(net, a, st.sparse0);
     if (t) {
       for (int l = 1; l <= L; ++l) d[l] = st.d[l].data() + p * net.n[l];
       st.sse_p[p] = backward_pattern(net, a.data(), d.data(), t + p * net.n[L]);
@@ -230,6 +236,7 @@ void batch_sum(const Net<Real>& net, const BatchState<Real>& st, int64_t rows, d
         const Real* dp = D + p * n_out;
         for (int i = r0; i < r1; ++i) {
           const double ai = (i < n_in) ? (double)A[p * n_in + i] : 1.0;
+          if (l == 0 && st.sparse0 && ai == 0.0) continue;
           double* g = Gl + (int64_t)i * n_out;
           for (int j = 0; j < n_out; ++j) g[j] += ai * (double)dp[j];
         }
@@ -326,6 +333,7 @@ void load_inputs(const Net<Real>& net, BatchState<Real>& st, int64_t p0, int64_t
                  const float* x, const int32_t* act, int n_active) {
   const int n0 = net.n[0];
   Real* a0 = st.a[0].data();
+  st.sparse0 = (x == nullptr);
   if (x) {
     for (int64_t p = 0; p < rows; ++p)
       for (int i = 0; i < n0; ++i) a0[p * n0 + i] = (Real)x[(p0 + p) * n0 + i];

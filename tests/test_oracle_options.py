@@ -168,16 +168,18 @@ def test_poisoned_target_faults_exactly_what_it_reaches_dense(poison):
     np.testing.assert_array_equal(W1[:, other], C1[:, other])
 
 
-def test_poisoned_target_faults_only_active_rows_onehot():
+@pytest.mark.parametrize("poison", [np.nan, 1e30])
+def test_poisoned_target_faults_only_active_rows_onehot(poison):
     # One-hot inputs: delta_1[p] reaches only the n_active rows of pattern p
     # and the bias row of W0: (n_active + 1) * H faults there, plus G1[:, k].
+    # (Inactive inputs take no part, so a NaN delta does not reach their rows.)
     n0, H, O, k_act = 30, 6, 4, 3
     sizes = (n0, H, O)
     g = np.random.default_rng(5)
     act = np.stack([g.choice(n0, k_act, replace=False) for _ in range(10)]).astype(np.int32)
     t = np.where(g.random((10, O)) < 0.5, 0.9, 0.1).astype(np.float32)
     w = g.uniform(-0.5, 0.5, wl.num_weights(sizes))
-    t[7, 2] = 1e30
+    t[7, 2] = poison
     net = _trained(sizes, w, None, t, 1e6, active=act)
     assert net.fault_count() == (H + 1) + (k_act + 1) * H
 
@@ -285,3 +287,19 @@ def test_guard_rejects_bad_arguments():
         net.guard_config(0, 1.5)
     with pytest.raises(oracle.OracleError):
         net.guard_config(1, 0.0)
+
+
+def test_onehot_first_layer_uses_only_active_rows():
+    # A non-finite weight in a row no pattern activates leaves one-hot outputs
+    # finite (the gather takes only the active rows), while the same inputs
+    # given densely meet it as 0 * NaN.
+    n0, H, O = 12, 4, 3
+    sizes = (n0, H, O)
+    g = np.random.default_rng(9)
+    act = np.array([[0, 3, 5], [1, 3, 7], [2, 4, 6]], np.int32)
+    w = g.uniform(-0.5, 0.5, wl.num_weights(sizes))
+    w[11 * H + 2] = np.nan                              # W0[11][2], row 11 never active
+    net = oracle.OracleNet(sizes, 64)
+    net.set_weights(w)
+    assert np.all(np.isfinite(net.forward(active=act)))
+    assert np.all(np.isnan(net.forward(x=wl.dense_from_active(act, n0))))
