@@ -122,6 +122,57 @@ int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* 
 int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, int64_t n_patterns,
                       float* outputs_dev);
 
+/* ---- Options of the method (all off after bp_create). */
+
+/* Unit nonlinearity (section 4.3).  BP_SIGMOID_EXACT: 1 / (1 + e^-x) in fp32
+ * (the default).  BP_SIGMOID_TABLE: the paper's second evaluation: x is taken
+ * to the nearest end of [-15, 15] when outside it, mapped onto [0, 255] as
+ * x1 = (x + 15) * 255 / 30, and the logistic is read from a 256-entry table
+ * of its values at -15 + 30 i / 255 (entry floor(x1)) with linear
+ * interpolation to the next entry by x1 - floor(x1); NaN stays NaN.  Maximum
+ * error 1.67e-4 (the linear-interpolation bound h^2 / 8 max|sigma''|).  The
+ * derivative used in the deltas stays y (1 - y).  Applies to every later
+ * train and forward call; waits for the net's stream. */
+enum { BP_SIGMOID_EXACT = 0, BP_SIGMOID_TABLE = 1 };
+int bp_set_sigmoid(bp_net* net, int32_t mode);
+
+/* Range check of the summed weight changes (section 8: each total weight
+ * change is tested for a reasonable range; one out of range is set to zero
+ * and counted as a fault).  limit > 0: every summed change G (the batch sum,
+ * before the learning rate) with |G| > limit or NaN is replaced by 0, so that
+ * weight moves by its momentum term only, and the fault counter is
+ * incremented.  limit == 0 disables the check.  Also resets the counter to 0.
+ * Returns BP_EINVAL for a negative or NaN limit.  Waits for the net's stream. */
+int bp_set_fault_limit(bp_net* net, float limit);
+
+/* Faults counted since the last bp_set_fault_limit (0 if never set).  Waits
+ * for the net's stream; *count is a host int64. */
+int bp_get_fault_count(bp_net* net, int64_t* count);
+
+/* In-HBM checkpoint of the weights and momentum (section 10.4): one slot
+ * owned by the net (allocated by the first save).  Save and restore are
+ * device-to-device copies enqueued on the net's stream.  Restore without a
+ * saved checkpoint returns BP_EINVAL. */
+int bp_checkpoint_save(bp_net* net);
+int bp_checkpoint_restore(bp_net* net);
+
+/* Rollback guard (section 10.4: copy weights to a checkpoint every few epochs
+ * and copy them back when the error jumps between epochs).  bp_guard_config
+ * saves a checkpoint now and arms the guard: every >= 1 accepted epochs
+ * between checkpoints, jump > 0 the error ratio that counts as a jump.  After
+ * each epoch the caller reports its summed squared error to bp_guard_epoch:
+ *   - if the error exceeds jump x the last accepted epoch's error (or is NaN),
+ *     W and V are restored from the checkpoint, *rolled_back = 1, and the
+ *     caller resumes from the checkpoint's epoch;
+ *   - otherwise the epoch is accepted (*rolled_back = 0), and every `every`
+ *     accepted epochs the checkpoint is renewed.
+ * A jump that recurs at the same epoch after a rollback is accepted: training
+ * is deterministic, so a jump that replays is the learning itself rather than
+ * a transient fault.  bp_guard_epoch without bp_guard_config returns
+ * BP_EINVAL. */
+int bp_guard_config(bp_net* net, int32_t every, double jump);
+int bp_guard_epoch(bp_net* net, double sse, int32_t* rolled_back);
+
 /* Measurement support (not part of the method).  Kernel kinds a net launches: */
 enum {
   BP_K_FORWARD = 0,   /* hidden-layer forward product + sigmoid            */

@@ -24,7 +24,10 @@ LIB_PATH = os.path.join(HERE, "libbp.so")
 BP_OK, BP_EINVAL, BP_ENOMEM, BP_EDEVICE = 0, -1, -2, -3
 EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set_weights", "bp_get_weights",
            "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
-           "bp_forward_onehot", "bp_profile", "bp_profile_report", "bp_last_error")
+           "bp_forward_onehot", "bp_set_sigmoid", "bp_set_fault_limit", "bp_get_fault_count",
+           "bp_checkpoint_save", "bp_checkpoint_restore", "bp_guard_config", "bp_guard_epoch", "bp_profile",
+           "bp_profile_report", "bp_last_error")
+BP_SIGMOID_EXACT, BP_SIGMOID_TABLE = 0, 1
 KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce", "fused_fb",
          "fused_update", "output_finish")
 
@@ -64,6 +67,13 @@ def lib():
                                                    ctypes.c_float, ctypes.c_float, _f64p]),
         "bp_forward": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, _vp]),
         "bp_forward_onehot": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int64, _vp]),
+        "bp_set_sigmoid": (ctypes.c_int, [_vp, ctypes.c_int32]),
+        "bp_set_fault_limit": (ctypes.c_int, [_vp, ctypes.c_float]),
+        "bp_get_fault_count": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64)]),
+        "bp_checkpoint_save": (ctypes.c_int, [_vp]),
+        "bp_checkpoint_restore": (ctypes.c_int, [_vp]),
+        "bp_guard_config": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double]),
+        "bp_guard_epoch": (ctypes.c_int, [_vp, ctypes.c_double, ctypes.POINTER(ctypes.c_int32)]),
         "bp_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
         "bp_profile_report": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64), _f64p, ctypes.c_int32]),
         "bp_last_error": (ctypes.c_char_p, [_vp]),
@@ -131,6 +141,40 @@ def bp_forward(h, inputs_ptr: int, n: int, outputs_ptr: int) -> int:
 
 def bp_forward_onehot(h, active_ptr: int, n_active: int, n: int, outputs_ptr: int) -> int:
     return lib().bp_forward_onehot(h, _vp(active_ptr), n_active, n, _vp(outputs_ptr))
+
+
+def bp_set_sigmoid(h, mode: int) -> int:
+    return lib().bp_set_sigmoid(h, int(mode))
+
+
+def bp_set_fault_limit(h, limit: float) -> int:
+    return lib().bp_set_fault_limit(h, float(limit))
+
+
+def bp_get_fault_count(h):
+    """Returns (rc, count)."""
+    c = ctypes.c_int64(0)
+    rc = lib().bp_get_fault_count(h, ctypes.byref(c))
+    return rc, int(c.value)
+
+
+def bp_checkpoint_save(h) -> int:
+    return lib().bp_checkpoint_save(h)
+
+
+def bp_checkpoint_restore(h) -> int:
+    return lib().bp_checkpoint_restore(h)
+
+
+def bp_guard_config(h, every: int, jump: float) -> int:
+    return lib().bp_guard_config(h, int(every), float(jump))
+
+
+def bp_guard_epoch(h, sse: float):
+    """Returns (rc, rolled_back)."""
+    r = ctypes.c_int32(0)
+    rc = lib().bp_guard_epoch(h, float(sse), ctypes.byref(r))
+    return rc, int(r.value)
 
 
 def bp_profile(h, on: bool) -> int:
@@ -223,6 +267,31 @@ class Net:
             rc = bp_train_batches(self._h, xp, tp, n, int(batch), float(lr), float(momentum), sse)
         self._chk(rc)
         return sse.value if want_sse else None
+
+    def set_sigmoid(self, mode: int) -> None:
+        self._chk(bp_set_sigmoid(self._h, mode))
+
+    def set_fault_limit(self, limit: float) -> None:
+        self._chk(bp_set_fault_limit(self._h, limit))
+
+    def fault_count(self) -> int:
+        rc, c = bp_get_fault_count(self._h)
+        self._chk(rc)
+        return c
+
+    def checkpoint_save(self) -> None:
+        self._chk(bp_checkpoint_save(self._h))
+
+    def checkpoint_restore(self) -> None:
+        self._chk(bp_checkpoint_restore(self._h))
+
+    def guard_config(self, every: int, jump: float) -> None:
+        self._chk(bp_guard_config(self._h, every, jump))
+
+    def guard_epoch(self, sse: float) -> int:
+        rc, r = bp_guard_epoch(self._h, sse)
+        self._chk(rc)
+        return r
 
     def profile(self, on: bool) -> None:
         self._chk(bp_profile(self._h, on))

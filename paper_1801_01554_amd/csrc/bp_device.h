@@ -1,0 +1,56 @@
+// bp_device.h -- device helpers shared by the gfx950 kernels: the unit
+// nonlinearity (exact or table, section 4.3) and the range check of summed
+// weight changes (section 8).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace bpk {
+
+// Table sigmoid geometry (section 4.3, figure 3): 256 entries, the logistic
+// at equally spaced points of [-15, 15]; [-15, 15] maps onto [0, 255] by
+// (z + 15) * 255 / 30, and 255 / 30 = 8.5 is exact in float.
+constexpr int kSigTableSize = 256;
+constexpr float kSigTableEnd = 15.0f;
+constexpr float kSigTableScale = 8.5f;
+
+__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
+
+// Inputs outside [-15, 15] take the end entries; inside, the integer part of
+// the mapped value picks an entry and the fractional part interpolates
+// linearly towards the next one.  NaN stays NaN.
+__device__ __forceinline__ float logistic_table(float z, const float* __restrict__ tab) {
+  if (z != z) return z;
+  const float zc = fminf(fmaxf(z, -kSigTableEnd), kSigTableEnd);
+  const float x1 = (zc + kSigTableEnd) * kSigTableScale;        // [0, 255]
+  const int i = min((int)x1, kSigTableSize - 2);                // x1 >= 0: truncation is the floor
+  const float f = x1 - (float)i;                                // 1 at x1 = 255: the last entry
+  const float a = tab[i], b = tab[i + 1];
+  return a + f * (b - a);
+}
+
+// The unit nonlinearity: the table when one is given, else the exact logistic.
+__device__ __forceinline__ float unit_sigma(float z, const float* __restrict__ tab) {
+  return tab ? logistic_table(z, tab) : logistic(z);
+}
+
+// Range check of one summed change: with limit > 0, a change outside
+// [-limit, limit] (or NaN) becomes 0 and is counted in `faults`.
+__device__ __forceinline__ float checked_change(float g, float limit, int& faults) {
+  if (limit > 0.f && !(fabsf(g) <= limit)) {
+    ++faults;
+    return 0.f;
+  }
+  return g;
+}
+
+// Adds the fault counts of a wave to the device counter: a wave sum, then one
+// atomic from lane 0 when the sum is nonzero.  Every lane of the wave must
+// reach this call.
+__device__ __forceinline__ void add_faults(int faults, unsigned long long* counter) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) faults += __shfl_xor(faults, off, 64);
+  if ((threadIdx.x & 63) == 0 && faults > 0) atomicAdd(counter, (unsigned long long)faults);
+}
+
+}  // namespace bpk

@@ -4,6 +4,13 @@
 // Matrices are fp32 row-major with an explicit leading dimension (in floats).
 // Weight layer l is stored as (n_l + 1) rows x ldw columns, ldw = n_{l+1}
 // rounded up to a multiple of 4; row n_l is the bias ("true unit") row.
+//
+// Options of the method, passed to the kernels they affect:
+//   tab            the 256-entry sigmoid table (section 4.3) in device memory,
+//                  or nullptr for the exact logistic;
+//   limit, faults  the range check of summed changes (section 8): with
+//                  limit > 0 every summed change outside [-limit, limit] (or
+//                  NaN) is replaced by 0 and counted in *faults (device).
 #pragma once
 
 #include <hip/hip_ext.h>
@@ -41,7 +48,7 @@ int colsum_rows(int M);
 
 // out[m][n] = sigma(sum_k A[m][k] W[k][n] + bias[n]),  m < M, n < N, k < K.
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
-                         int K, const float* bias, float* out, int ldo);
+                         int K, const float* bias, float* out, int ldo, const float* tab);
 
 // Output layer during training: y = sigma(A W + bias); e = T - y;
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of
@@ -54,9 +61,9 @@ int output_delta_splits(int M, int N, int K);
 size_t output_delta_workspace(int M, int N, int K);
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M,
                                 int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                                int ldd, double* sse_part, float* colsum, int ldcs, float* ws);
+                                int ldd, double* sse_part, float* colsum, int ldcs, float* ws, const float* tab);
 hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws);
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab);
 
 // Hidden deltas: out[m][n] = (sum_k D[m][k] W[n][k]) * act[m][n] (1 - act[m][n]),
 // with W rows n < N the non-bias rows of the layer above (ldw floats apart);
@@ -76,16 +83,17 @@ size_t change_update_workspace(int M, int N, int K);
 // With change_splits(M, N, K) > 1 this launch only writes the partial sums
 // to `ws` (change_update_workspace floats) and splitk_finish must follow.
 hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N,
-                         int K, float* W, float* V, int ldw, float lr, float mom, float* ws);
+                         int K, float* W, float* V, int ldw, float lr, float mom, float* ws, float limit,
+                         unsigned long long* faults);
 
 // Sums the split partials of change_update in split order, then updates V and W.
 hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
-                         const float* ws);
+                         const float* ws, float limit, unsigned long long* faults);
 
 // Bias-row change and update: G[n] = sum_{k < rows} D[k][n];  V = lr G + mom V;  W += V.
 // D is the per-tile column-sum buffer of the deltas (rows = colsum_rows(batch)).
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb,
-                       float lr, float mom);
+                       float lr, float mom, float limit, unsigned long long* faults);
 
 // One-hot first layer: net[p][j] = W0[n0][j] + sum_{k < n_active} W0[act[p][k]][j].
 // mode 0: out[p][j] = sigma(net).  mode 1 (single-layer nets, training):
@@ -94,13 +102,14 @@ hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, 
 int onehot_forward_blocks(int rows, int H);
 hipError_t onehot_forward(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw,
                           int n0, int H, int mode, float* out, int ldo, const float* T, int ldt,
-                          double* sse_part);
+                          double* sse_part, const float* tab);
 
 // One-hot first-layer change and update for all n0 + 1 rows:
 //   G[r][j] = sum over patterns p containing index r of D[p][j]  (r < n0),
 //   G[n0][j] = sum_p D[p][j];  V = lr G + mom V;  W += V.
 hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* D, int ldd,
-                         int n0, int H, float* W, float* V, int ldw, float lr, float mom);
+                         int n0, int H, float* W, float* V, int ldw, float lr, float mom, float limit,
+                         unsigned long long* faults);
 
 // ---- fused path for small two-layer nets with one-hot inputs (bp_small.hip)
 constexpr int kSmallMaxHidden = 256;
@@ -117,12 +126,12 @@ int small_fwdbwd_blocks(int rows);
 // D2 = (T - Y) Y (1 - Y), D1 = (D2 W1^T) A1 (1 - A1); error partials per block.
 hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
                         int H, const float* W1, int ldw1, int O, const float* T, float* A1, int lda1, float* D1,
-                        float* D2, int ldd2, double* sse_part);
+                        float* D2, int ldd2, double* sse_part, const float* tab);
 
 // Summed changes of both layers over the batch and the momentum update of all weights.
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
                         int lda1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                        float* V1, int ldw1, int O, float lr, float mom);
+                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults);
 
 // out[0] = sum of part[0 .. n-1] in a fixed order (double).
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out);

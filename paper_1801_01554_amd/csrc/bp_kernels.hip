@@ -14,6 +14,7 @@
 // Every reduction runs in a fixed order: results are run-to-run identical.
 #include <hip/hip_runtime.h>
 
+#include "bp_device.h"
 #include "bp_internal.h"
 
 namespace bpk {
@@ -24,25 +25,28 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
 
-__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
-
 // --------------------------------------------------------------------------
 // Epilogues.  apply() gets one element of the product (row m, column n) plus
 // the per-column value column() returned, and returns the value that enters
-// the per-tile column sums; kSSE marks epilogues that add to a per-block
-// squared-error partial, kColSum those that write per-tile column sums of
-// the deltas they produce (colsum[tile row][n]; the bias-row change of the
-// layer below is the sum of these over the tile rows).
+// the per-tile column sums; its last argument is a per-lane statistic: the
+// squared error for kSSE epilogues (added into a per-block partial), the
+// number of range-check faults for kFaults epilogues (added to the fault
+// counter).  kColSum marks epilogues that write per-tile column sums of the
+// deltas they produce (colsum[tile row][n]; the bias-row change of the layer
+// below is the sum of these over the tile rows).  `tab` is the sigmoid table
+// (nullptr: exact logistic).
 
 struct EpiSigmoid {
   const float* bias;
   float* out;
   int ldo;
+  const float* tab;
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
+  static constexpr bool kFaults = false;
   __device__ float column(int n) const { return bias[n]; }
   __device__ float apply(int m, int n, float acc, float b, float&) const {
-    out[(size_t)m * ldo + n] = logistic(acc + b);
+    out[(size_t)m * ldo + n] = unit_sigma(acc + b, tab);
     return 0.f;
   }
 };
@@ -56,11 +60,13 @@ struct EpiOutputDelta {
   double* sse_part;
   float* colsum;
   int ldcs;
+  const float* tab;
   static constexpr bool kSSE = true;
   static constexpr bool kColSum = true;
+  static constexpr bool kFaults = false;
   __device__ float column(int n) const { return bias[n]; }
   __device__ float apply(int m, int n, float acc, float b, float& sse) const {
-    const float y = logistic(acc + b);
+    const float y = unit_sigma(acc + b, tab);
     const float e = T[(size_t)m * ldt + n] - y;
     sse += e * e;
     const float d = e * y * (1.0f - y);
@@ -78,6 +84,7 @@ struct EpiHiddenDelta {
   int ldcs;
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = true;
+  static constexpr bool kFaults = false;
   __device__ float column(int) const { return 0.f; }
   __device__ float apply(int m, int n, float acc, float, float&) const {
     const float a = act[(size_t)m * lda + n];
@@ -92,12 +99,18 @@ struct EpiUpdate {
   float* V;
   int ldw;
   float lr, mom;
+  float limit;                      // range check of the summed change (> 0: on)
+  unsigned long long* faults;
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
+  static constexpr bool kFaults = true;
   __device__ float column(int) const { return 0.f; }
-  __device__ float apply(int m, int n, float acc, float, float&) const {
+  __device__ float apply(int m, int n, float acc, float, float& nf) const {
     const size_t i = (size_t)m * ldw + n;
-    const float v = lr * acc + mom * V[i];
+    int f = 0;
+    const float g = checked_change(acc, limit, f);
+    nf += (float)f;
+    const float v = lr * g + mom * V[i];
     V[i] = v;
     W[i] = W[i] + v;
     return 0.f;
@@ -111,6 +124,7 @@ struct EpiPartial {
   size_t split_stride;
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
+  static constexpr bool kFaults = false;
   __device__ float column(int) const { return 0.f; }
   __device__ float apply(int m, int n, float acc, float, float&) const {
     P[blockIdx.z * split_stride + (size_t)m * ldp + n] = acc;
@@ -326,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
-  float sse = 0.f;
+  float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
   float csum[T::TN];
 #pragma unroll
   for (int j = 0; j < T::TN; ++j) {
@@ -367,6 +381,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
         epi.colsum[(size_t)crow * epi.ldcs + n0 + c] = v;
       }
     }
+  }
+  if constexpr (Epi::kFaults) {
+    if (epi.limit > 0.f) add_faults((int)sse, epi.faults);
   }
   if constexpr (Epi::kSSE) {
     __shared__ float red[kThreads / 64];
@@ -422,16 +439,21 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __restrict__ P, int splits,
                                                                  size_t split_stride, int M, int N, int ldp,
                                                                  float* W, float* V, int ldw, float lr,
-                                                                 float mom) {
+                                                                 float mom, float limit,
+                                                                 unsigned long long* faults) {
   const size_t idx = (size_t)blockIdx.x * kThreads + threadIdx.x;
-  if (idx >= (size_t)M * N) return;
-  const int m = (int)(idx / N), n = (int)(idx % N);
-  float g = 0.f;
-  for (int z = 0; z < splits; ++z) g += P[z * split_stride + (size_t)m * ldp + n];
-  const size_t i = (size_t)m * ldw + n;
-  const float v = lr * g + mom * V[i];
-  V[i] = v;
-  W[i] = W[i] + v;
+  int nf = 0;
+  if (idx < (size_t)M * N) {
+    const int m = (int)(idx / N), n = (int)(idx % N);
+    float g = 0.f;
+    for (int z = 0; z < splits; ++z) g += P[z * split_stride + (size_t)m * ldp + n];
+    g = checked_change(g, limit, nf);
+    const size_t i = (size_t)m * ldw + n;
+    const float v = lr * g + mom * V[i];
+    V[i] = v;
+    W[i] = W[i] + v;
+  }
+  if (limit > 0.f) add_faults(nf, faults);
 }
 
 // Split-K output layer: sums the split partials in split order, then applies
@@ -444,7 +466,8 @@ constexpr int kFin = 1024;
 __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __restrict__ P, int splits, size_t stride,
                                                              int ldp, int M, int N, const float* __restrict__ bias,
                                                              const float* __restrict__ T, int ldt, float* delta,
-                                                             int ldd, double* sse_part, float* colsum, int ldcs) {
+                                                             int ldd, double* sse_part, float* colsum, int ldcs,
+                                                             const float* __restrict__ tab) {
   constexpr int W = kFin / 64, R = 128 / W;
   __shared__ float cs[W][64];
   __shared__ float red[W];
@@ -470,7 +493,7 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       if (m0 + r >= M) break;
-      const float y = logistic(z[r] + b);
+      const float y = unit_sigma(z[r] + b, tab);
       const float e = t[r] - y;
       sse += e * e;
       const float d = e * y * (1.0f - y);
@@ -501,7 +524,8 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
 constexpr int kBiasWaves = 16;
 __global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(const float* __restrict__ D, int ldd,
                                                                        int rows, int N, float* Wb, float* Vb,
-                                                                       float lr, float mom) {
+                                                                       float lr, float mom, float limit,
+                                                                       unsigned long long* faults) {
   __shared__ float part[kBiasWaves][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n = blockIdx.x * 64 + lane;
@@ -521,12 +545,17 @@ __global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(const floa
   }
   part[wave][lane] = s;
   __syncthreads();
-  if (wave == 0 && n < N) {
-    float g = 0.f;
-    for (int w = 0; w < kBiasWaves; ++w) g += part[w][lane];
-    const float v = lr * g + mom * Vb[n];
-    Vb[n] = v;
-    Wb[n] = Wb[n] + v;
+  if (wave == 0) {
+    int nf = 0;
+    if (n < N) {
+      float g = 0.f;
+      for (int w = 0; w < kBiasWaves; ++w) g += part[w][lane];
+      g = checked_change(g, limit, nf);
+      const float v = lr * g + mom * Vb[n];
+      Vb[n] = v;
+      Wb[n] = Wb[n] + v;
+    }
+    if (limit > 0.f) add_faults(nf, faults);
   }
 }
 
@@ -535,7 +564,7 @@ __global__ __launch_bounds__(kThreads) void onehot_forward_kernel(const int32_t*
                                                                   int rows, const float* __restrict__ W0, int ldw,
                                                                   int n0, int H, int strips, int mode, float* out,
                                                                   int ldo, const float* __restrict__ T, int ldt,
-                                                                  double* sse_part) {
+                                                                  double* sse_part, const float* __restrict__ tab) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int item = blockIdx.x * (kThreads / 64) + wave;
   const int p = item / strips, col = (item % strips) * 64 + lane;
@@ -544,7 +573,7 @@ __global__ __launch_bounds__(kThreads) void onehot_forward_kernel(const int32_t*
     float net = W0[(size_t)n0 * ldw + col];
     const int32_t* a = act + (size_t)p * n_active;
     for (int k = 0; k < n_active; ++k) net += W0[(size_t)a[k] * ldw + col];
-    const float y = logistic(net);
+    const float y = unit_sigma(net, tab);
     if (mode == 0) {
       out[(size_t)p * ldo + col] = y;
     } else {
@@ -573,7 +602,8 @@ __global__ __launch_bounds__(kThreads) void onehot_forward_kernel(const int32_t*
 __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* __restrict__ act, int n_active,
                                                                  int rows, const float* __restrict__ D, int ldd,
                                                                  int n0, int H, float* W, float* V, int ldw,
-                                                                 float lr, float mom) {
+                                                                 float lr, float mom, float limit,
+                                                                 unsigned long long* faults) {
   __shared__ int list[kThreads];
   __shared__ int wave_cnt[kThreads / 64];
   const int r = blockIdx.x;
@@ -608,12 +638,15 @@ __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* 
       for (int q = 0; q < total; ++q) g += D[(size_t)list[q] * ldd + col];
     __syncthreads();
   }
+  int nf = 0;
   if (col < H) {
+    g = checked_change(g, limit, nf);
     const size_t i = (size_t)r * ldw + col;
     const float v = lr * g + mom * V[i];
     V[i] = v;
     W[i] = W[i] + v;
   }
+  if (limit > 0.f) add_faults(nf, faults);
 }
 
 // Fixed-order sum of n doubles by one block of 1024 threads: thread t adds
@@ -682,17 +715,17 @@ size_t output_delta_workspace(int M, int N, int K) {
 int output_delta_splits(int M, int N, int K) { return choose_output_splits(M, N, K); }
 
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
-                         const float* bias, float* out, int ldo) {
-  EpiSigmoid e{bias, out, ldo};
+                         const float* bias, float* out, int ldo, const float* tab) {
+  EpiSigmoid e{bias, out, ldo, tab};
   return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
 }
 
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
                                 const float* bias, const float* T, int ldt, float* delta, int ldd, double* sse_part,
-                                float* colsum, int ldcs, float* ws) {
+                                float* colsum, int ldcs, float* ws, const float* tab) {
   const int sp = choose_output_splits(M, N, K);
   if (sp <= 1) {
-    EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs};
+    EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs, tab};
     return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
@@ -701,13 +734,13 @@ hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const fl
 }
 
 hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws) {
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab) {
   const int sp = choose_output_splits(M, N, K);
   if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
   const int ldp = (N + 3) / 4 * 4;
   dim3 grid((M + 127) / 128, (N + 63) / 64);
   return launch_kernel(output_finish_kernel, grid, kFin, 0, s, ws, sp, (size_t)M * ldp, ldp, M, N, bias, T, ldt,
-                       delta, ldd, sse_part, colsum, ldcs);
+                       delta, ldd, sse_part, colsum, ldcs, tab);
 }
 
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,
@@ -726,11 +759,12 @@ size_t change_update_workspace(int M, int N, int K) {
 }
 
 hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N, int K,
-                         float* W, float* V, int ldw, float lr, float mom, float* ws) {
+                         float* W, float* V, int ldw, float lr, float mom, float* ws, float limit,
+                         unsigned long long* faults) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const int sp = choose_splits(M, N, K);
   if (sp <= 1) {
-    EpiUpdate e{W, V, ldw, lr, mom};
+    EpiUpdate e{W, V, ldw, lr, mom, limit, faults};
     return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
@@ -739,19 +773,20 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
 }
 
 hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
-                         const float* ws) {
+                         const float* ws, float limit, unsigned long long* faults) {
   const int sp = choose_splits(M, N, K);
   if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
   const int ldp = (N + 3) / 4 * 4;
   const size_t total = (size_t)M * N;
   return launch_kernel(splitk_update_kernel, (unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s, 
-      ws, sp, (size_t)M * ldp, M, N, ldp, W, V, ldw, lr, mom);
+      ws, sp, (size_t)M * ldp, M, N, ldp, W, V, ldw, lr, mom, limit, faults);
 }
 
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb, float lr,
-                       float mom) {
+                       float mom, float limit, unsigned long long* faults) {
   if (N <= 0) return hipSuccess;
-  return launch_kernel(bias_update_kernel, (N + 63) / 64, 64 * kBiasWaves, 0, s, D, ldd, rows, N, Wb, Vb, lr, mom);
+  return launch_kernel(bias_update_kernel, (N + 63) / 64, 64 * kBiasWaves, 0, s, D, ldd, rows, N, Wb, Vb, lr, mom,
+                       limit, faults);
 }
 
 int onehot_forward_blocks(int rows, int H) {
@@ -761,18 +796,21 @@ int onehot_forward_blocks(int rows, int H) {
 }
 
 hipError_t onehot_forward(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw,
-                          int n0, int H, int mode, float* out, int ldo, const float* T, int ldt, double* sse_part) {
+                          int n0, int H, int mode, float* out, int ldo, const float* T, int ldt, double* sse_part,
+                          const float* tab) {
   if (rows <= 0 || H <= 0) return hipSuccess;
   const int strips = (H + 63) / 64;
   return launch_kernel(onehot_forward_kernel, onehot_forward_blocks(rows, H), kThreads, 0, s, act, n_active, rows, W0, ldw, n0, H,
-                                                                            strips, mode, out, ldo, T, ldt, sse_part);
+                                                                            strips, mode, out, ldo, T, ldt, sse_part, tab);
 }
 
 hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* D, int ldd, int n0,
-                         int H, float* W, float* V, int ldw, float lr, float mom) {
+                         int H, float* W, float* V, int ldw, float lr, float mom, float limit,
+                         unsigned long long* faults) {
   if (H <= 0) return hipSuccess;
   dim3 grid(n0 + 1, (H + kThreads - 1) / kThreads);
-  return launch_kernel(onehot_update_kernel, grid, kThreads, 0, s, act, n_active, rows, D, ldd, n0, H, W, V, ldw, lr, mom);
+  return launch_kernel(onehot_update_kernel, grid, kThreads, 0, s, act, n_active, rows, D, ldd, n0, H, W, V, ldw, lr,
+                       mom, limit, faults);
 }
 
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out) {

@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -44,6 +45,25 @@ struct bp_net {
   double* sse_part = nullptr;
   size_t sse_cap = 0;
   double* sse_dev = nullptr;
+  // options (section 4.3 table sigmoid; section 8 range check)
+  float* sig_tab = nullptr;           // device table, set while the table sigmoid is selected
+  float* sig_tab_mem = nullptr;       // its allocation (kept once made)
+  float fault_limit = 0.f;            // > 0: range check on
+  unsigned long long* faults = nullptr;
+  // checkpoint of W and V (section 10.4) and the guard that uses it
+  float* ckW = nullptr;
+  float* ckV = nullptr;
+  struct Guard {
+    bool on = false;
+    int every = 1;
+    double jump = 0.0;
+    int since = 0;                    // epochs accepted since the checkpoint
+    int retry_at = -1;                // epoch (from the checkpoint) already rolled back once
+    bool have_last = false;
+    double last_sse = 0.0;            // error of the last accepted epoch
+    bool ck_have = false;
+    double ck_sse = 0.0;              // error of the epoch the checkpoint was taken at
+  } guard;
   // measurement: launches bracketed by events while `prof` is set
   bool prof = false;
   struct Rec {
@@ -209,7 +229,7 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
     if (l == 0 && in.act) {
       BP_LAUNCH(net, BP_K_GATHER,
                 bpk::onehot_forward(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], net->n[0], net->n[1],
-                                    (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part));
+                                    (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part, net->sig_tab));
       continue;
     }
     const float* A = (l == 0) ? in.x : acts[l];
@@ -218,15 +238,15 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
       BP_LAUNCH(net, BP_K_OUTPUT,
                 bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
                                           wbias(net, l), T, net->n[L], dst, ldd, sse_part, net->csum[L],
-                                          net->lda[L], net->splitk));
+                                          net->lda[L], net->splitk, net->sig_tab));
       if (bpk::output_delta_splits(rows, net->n[l + 1], net->n[l]) > 1)
         BP_LAUNCH(net, BP_K_OUTFIN,
                   bpk::output_finish(s, rows, net->n[l + 1], net->n[l], wbias(net, l), T, net->n[L], dst, ldd,
-                                     sse_part, net->csum[L], net->lda[L], net->splitk));
+                                     sse_part, net->csum[L], net->lda[L], net->splitk, net->sig_tab));
     } else
       BP_LAUNCH(net, BP_K_FORWARD,
                 bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
-                                   wbias(net, l), dst, ldd));
+                                   wbias(net, l), dst, ldd, net->sig_tab));
   }
   return BP_OK;
 }
@@ -248,11 +268,12 @@ int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, doubl
   const int n0 = net->n[0], H = net->n[1], O = net->n[2];
   BP_LAUNCH(net, BP_K_FUSED_FB,
             bpk::small_fwdbwd(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], n0, H, wl(net, 1), net->ldw[1], O,
-                              T, net->act[1], net->lda[1], net->del[1], net->del[2], net->lda[2], sse_part));
+                              T, net->act[1], net->lda[1], net->del[1], net->del[2], net->lda[2], sse_part,
+                              net->sig_tab));
   BP_LAUNCH(net, BP_K_FUSED_UPD,
             bpk::small_update(s, in.act, in.n_active, rows, net->act[1], net->del[1], net->lda[1], net->del[2],
                               net->lda[2], wl(net, 0), vl(net, 0), net->ldw[0], n0, H, wl(net, 1), vl(net, 1),
-                              net->ldw[1], O, lr, mom));
+                              net->ldw[1], O, lr, mom, net->fault_limit, net->faults));
   return BP_OK;
 }
 
@@ -270,21 +291,22 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
     if (l == 0 && in.act) {
       BP_LAUNCH(net, BP_K_SCATTER,
                 bpk::onehot_update(s, in.act, in.n_active, rows, net->del[1], net->lda[1], net->n[0], net->n[1],
-                                   wl(net, 0), vl(net, 0), net->ldw[0], lr, mom));
+                                   wl(net, 0), vl(net, 0), net->ldw[0], lr, mom, net->fault_limit, net->faults));
       continue;
     }
     const float* A = (l == 0) ? in.x : net->act[l];
     const int ldA = (l == 0) ? net->n[0] : net->lda[l];
     BP_LAUNCH(net, BP_K_CHANGE,
               bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
-                                 wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk));
+                                 wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk, net->fault_limit,
+                                 net->faults));
     if (bpk::change_splits(net->n[l], net->n[l + 1], rows) > 1)
       BP_LAUNCH(net, BP_K_SPLITK,
                 bpk::splitk_finish(s, net->n[l], net->n[l + 1], rows, wl(net, l), vl(net, l), net->ldw[l], lr, mom,
-                                   net->splitk));
+                                   net->splitk, net->fault_limit, net->faults));
     BP_LAUNCH(net, BP_K_BIAS,
               bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1], bpk::colsum_rows(rows), net->n[l + 1],
-                               wbias(net, l), vbias(net, l), lr, mom));
+                               wbias(net, l), vbias(net, l), lr, mom, net->fault_limit, net->faults));
   }
   return BP_OK;
 }
@@ -363,6 +385,30 @@ int forward_only(bp_net* net, const BatchInput& in, int64_t n, float* out) {
   return BP_OK;
 }
 
+int checkpoint_save(bp_net* net) {
+  const size_t bytes = sizeof(float) * net->wtotal;
+  if (!net->ckW) {
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+    BP_HIP(net, hipMalloc(&net->ckW, bytes));
+    const hipError_t e = hipMalloc(&net->ckV, bytes);
+    if (e != hipSuccess) {
+      free_ptr(net->ckW);
+      net->ckW = nullptr;
+      return hip_fail(net, e, "hipMalloc(checkpoint)");
+    }
+  }
+  BP_HIP(net, hipMemcpyAsync(net->ckW, net->W, bytes, hipMemcpyDeviceToDevice, net->stream));
+  BP_HIP(net, hipMemcpyAsync(net->ckV, net->V, bytes, hipMemcpyDeviceToDevice, net->stream));
+  return BP_OK;
+}
+
+int checkpoint_restore(bp_net* net) {
+  const size_t bytes = sizeof(float) * net->wtotal;
+  BP_HIP(net, hipMemcpyAsync(net->W, net->ckW, bytes, hipMemcpyDeviceToDevice, net->stream));
+  BP_HIP(net, hipMemcpyAsync(net->V, net->ckV, bytes, hipMemcpyDeviceToDevice, net->stream));
+  return BP_OK;
+}
+
 int check_net(bp_net* net) { return net ? BP_OK : BP_EINVAL; }
 
 }  // namespace
@@ -420,6 +466,10 @@ void bp_destroy(bp_net* net) {
   free_ptr(net->fwd_tmp[1]);
   free_ptr(net->sse_part);
   free_ptr(net->sse_dev);
+  free_ptr(net->sig_tab_mem);
+  free_ptr(net->faults);
+  free_ptr(net->ckW);
+  free_ptr(net->ckV);
   free_ptr(net->W);
   free_ptr(net->V);
   for (auto& r : net->recs) {
@@ -566,6 +616,110 @@ int bp_profile_report(bp_net* net, int64_t* launches, double* ms, int32_t n_kind
     launches[k] = net->prof_n[k];
     ms[k] = net->prof_ms[k];
   }
+  return BP_OK;
+}
+
+int bp_set_sigmoid(bp_net* net, int32_t mode) {
+  if (check_net(net)) return BP_EINVAL;
+  if (mode != BP_SIGMOID_EXACT && mode != BP_SIGMOID_TABLE)
+    return fail(net, BP_EINVAL, "bp_set_sigmoid: mode must be BP_SIGMOID_EXACT or BP_SIGMOID_TABLE");
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  if (mode == BP_SIGMOID_EXACT) {
+    net->sig_tab = nullptr;
+    return BP_OK;
+  }
+  if (!net->sig_tab_mem) {
+    // entry i: the logistic at -15 + 30 i / 255, evaluated in double (section 4.3)
+    float host[256];
+    for (int i = 0; i < 256; ++i) {
+      const double x = -15.0 + 30.0 * (double)i / 255.0;
+      host[i] = (float)(1.0 / (1.0 + std::exp(-x)));
+    }
+    BP_HIP(net, hipMalloc(&net->sig_tab_mem, sizeof(host)));
+    BP_HIP(net, hipMemcpy(net->sig_tab_mem, host, sizeof(host), hipMemcpyHostToDevice));
+  }
+  net->sig_tab = net->sig_tab_mem;
+  return BP_OK;
+}
+
+int bp_set_fault_limit(bp_net* net, float limit) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!(limit >= 0.f)) return fail(net, BP_EINVAL, "bp_set_fault_limit: limit must be >= 0");
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  if (!net->faults) BP_HIP(net, hipMalloc(&net->faults, sizeof(unsigned long long)));
+  const unsigned long long zero = 0;
+  BP_HIP(net, hipMemcpy(net->faults, &zero, sizeof(zero), hipMemcpyHostToDevice));
+  net->fault_limit = limit;
+  return BP_OK;
+}
+
+int bp_get_fault_count(bp_net* net, int64_t* count) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!count) return fail(net, BP_EINVAL, "bp_get_fault_count: count is NULL");
+  unsigned long long c = 0;
+  if (net->faults) {
+    BP_HIP(net, hipMemcpyAsync(&c, net->faults, sizeof(c), hipMemcpyDeviceToHost, net->stream));
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+  }
+  *count = (int64_t)c;
+  return BP_OK;
+}
+
+int bp_checkpoint_save(bp_net* net) {
+  if (check_net(net)) return BP_EINVAL;
+  return checkpoint_save(net);
+}
+
+int bp_checkpoint_restore(bp_net* net) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!net->ckW) return fail(net, BP_EINVAL, "bp_checkpoint_restore: no checkpoint saved");
+  return checkpoint_restore(net);
+}
+
+int bp_guard_config(bp_net* net, int32_t every, double jump) {
+  if (check_net(net)) return BP_EINVAL;
+  if (every < 1 || !(jump > 0.0)) return fail(net, BP_EINVAL, "bp_guard_config: need every >= 1 and jump > 0");
+  const int rc = checkpoint_save(net);
+  if (rc) return rc;
+  net->guard = bp_net::Guard();
+  net->guard.on = true;
+  net->guard.every = every;
+  net->guard.jump = jump;
+  return BP_OK;
+}
+
+int bp_guard_epoch(bp_net* net, double sse, int32_t* rolled_back) {
+  if (check_net(net)) return BP_EINVAL;
+  if (!rolled_back) return fail(net, BP_EINVAL, "bp_guard_epoch: rolled_back is NULL");
+  if (!net->guard.on) return fail(net, BP_EINVAL, "bp_guard_epoch: call bp_guard_config first");
+  bp_net::Guard& g = net->guard;
+  const int pos = g.since + 1;
+  // a NaN error compares false: it counts as a jump
+  const bool jumped = g.have_last && !(sse <= g.jump * g.last_sse);
+  if (jumped && g.retry_at != pos) {
+    const int rc = checkpoint_restore(net);
+    if (rc) return rc;
+    g.retry_at = pos;
+    g.since = 0;
+    g.have_last = g.ck_have;
+    g.last_sse = g.ck_sse;
+    *rolled_back = 1;
+    return BP_OK;
+  }
+  // accepted (a jump that recurs at the epoch already rolled back is the
+  // learning itself: the replay is deterministic)
+  g.have_last = true;
+  g.last_sse = sse;
+  g.since = pos;
+  if (g.since == g.every) {
+    const int rc = checkpoint_save(net);
+    if (rc) return rc;
+    g.ck_have = true;
+    g.ck_sse = sse;
+    g.since = 0;
+    g.retry_at = -1;
+  }
+  *rolled_back = 0;
   return BP_OK;
 }
 

@@ -21,6 +21,7 @@
 // grouping of the work differs from the generic path.
 #include <hip/hip_runtime.h>
 
+#include "bp_device.h"
 #include "bp_internal.h"
 
 namespace bpk {
@@ -33,8 +34,6 @@ constexpr int kMaxP = 8;       // patterns per forward/backward block
 constexpr int kStageFloats = 32768;   // LDS floats the update blocks stage batch chunks in
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
 
 // q / d and q % d for 0 <= q < 2^16 and 1 <= d <= 2^10, through a float
 // reciprocal: the float quotient is within 2^-8 / d of the true one, far from
@@ -51,15 +50,17 @@ __device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int&
 //
 // The kernel has two rounds of global loads: (1) indices, targets and W1,
 // all independent; (2) the gathered W0 rows of all the block's patterns.
-// P (patterns per block) is a template parameter so that each instantiation
-// holds only the unrolled code it runs: these kernels are short enough that
-// instruction-cache misses at launch are a visible part of their time.
-template <int P>
+// P (patterns per block) and TAB (table sigmoid) are template parameters so
+// that each instantiation holds only the code it runs: these kernels are
+// short enough that instruction-cache misses at launch are a visible part of
+// their time.
+template <int P, bool TAB>
 __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                           const float* __restrict__ W0, int ldw0, int n0,
                                                           int H, const float* __restrict__ W1, int ldw1, int O,
                                                           const float* __restrict__ T, float* A1, int lda1,
-                                                          float* D1, float* D2, int ldd2, double* sse_part) {
+                                                          float* D1, float* D2, int ldd2, double* sse_part,
+                                                          const float* __restrict__ tab) {
   extern __shared__ float smem[];
   const int S1 = O + 1;
   float* w1s = smem;                                         // (H + 1) x S1
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       for (int u = 0; u < 8; ++u)
         if (u < n_active) net += v[p][u];
       for (int k = 8; k < n_active; ++k) net += W0[(size_t)idx[p * n_active + k] * ldw0 + j];
-      const float h = logistic(net);
+      const float h = TAB ? logistic_table(net, tab) : logistic(net);
       hs[p * H + j] = h;
       A1[(size_t)(p0 + p) * lda1 + j] = h;
     }
@@ -160,7 +161,8 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       }
       for (int m = 1; m < lpo; m <<= 1) z += __shfl_xor(z, m, 64);
       if (q < nout && part == 0) {
-        const float y = logistic(w1s[H * S1 + c] + z);
+        const float zo = w1s[H * S1 + c] + z;
+        const float y = TAB ? logistic_table(zo, tab) : logistic(zo);
         const float e = ts[q] - y;
         sse += e * e;
         const float d = e * y * (1.0f - y);
@@ -216,12 +218,14 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
 //   (w / 4) of each compacted list.
 // Blocks [nA + n0, nA + n0 + nS): the bias row of W0, 64 columns per block:
 //   sum_p D1[p][j].
+// CHECK: the range check of the summed changes (limit > 0).
+template <bool CHECK>
 __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                            const float* __restrict__ A1, const float* __restrict__ D1,
                                                            int lda1, const float* __restrict__ D2, int ldd2,
                                                            float* W0, float* V0, int ldw0, int n0, int H, float* W1,
                                                            float* V1, int ldw1, int O, int nA, int ch, float lr,
-                                                           float mom) {
+                                                           float mom, float limit, unsigned long long* faults) {
   extern __shared__ float stage[];
   __shared__ float part[kWU][64];
   __shared__ int list[kTU];
@@ -402,10 +406,15 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       for (int w = 1; w < kWU; ++w) g += part[w][lane];
     }
   }
-  if (owner && live) {
-    const float v = lr * g + mom * v_old;
-    Vt[col] = v;
-    Wt[col] = w_old + v;
+  if (owner) {   // whole waves
+    int nf = 0;
+    if (live) {
+      if (CHECK) g = checked_change(g, limit, nf);
+      const float v = lr * g + mom * v_old;
+      Vt[col] = v;
+      Wt[col] = w_old + v;
+    }
+    if (CHECK) add_faults(nf, faults);
   }
 }
 
@@ -428,25 +437,36 @@ int small_fwdbwd_blocks(int rows) {
   return (rows + P - 1) / P;
 }
 
+template <bool TAB>
+hipError_t launch_fwdbwd(hipStream_t s, int P, int nb, size_t lds, const int32_t* act, int n_active, int rows,
+                         const float* W0, int ldw0, int n0, int H, const float* W1, int ldw1, int O, const float* T,
+                         float* A1, int lda1, float* D1, float* D2, int ldd2, double* sse_part, const float* tab) {
+  switch (P) {
+    case 1: return launch_kernel(small_fwdbwd_kernel<1, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
+    case 2: return launch_kernel(small_fwdbwd_kernel<2, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
+    case 4: return launch_kernel(small_fwdbwd_kernel<4, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
+    default: return launch_kernel(small_fwdbwd_kernel<8, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
+  }
+}
+
 hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
                         int H, const float* W1, int ldw1, int O, const float* T, float* A1, int lda1, float* D1,
-                        float* D2, int ldd2, double* sse_part) {
+                        float* D2, int ldd2, double* sse_part, const float* tab) {
   if (rows <= 0) return hipSuccess;
   const int P = patterns_per_block(rows);
   const size_t lds = sizeof(float) * ((size_t)(H + 1) * (O + 1) + (size_t)P * H + 2 * (size_t)P * O) +
                      sizeof(int) * (size_t)P * n_active;
   const int nb = small_fwdbwd_blocks(rows);
-  switch (P) {
-    case 1: return launch_kernel(small_fwdbwd_kernel<1>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
-    case 2: return launch_kernel(small_fwdbwd_kernel<2>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
-    case 4: return launch_kernel(small_fwdbwd_kernel<4>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
-    default: return launch_kernel(small_fwdbwd_kernel<8>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part);
-  }
+  if (tab)
+    return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2,
+                               ldd2, sse_part, tab);
+  return launch_fwdbwd<false>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2,
+                              ldd2, sse_part, tab);
 }
 
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
                         int lda1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                        float* V1, int ldw1, int O, float lr, float mom) {
+                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults) {
   if (rows <= 0) return hipSuccess;
   const int nA = ((H + 1) * O + 63) / 64;
   const int nS = (H + 63) / 64;
@@ -457,8 +477,11 @@ hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int row
   int ch = 1;
   while (ch * 2 * per <= kStageFloats) ch *= 2;
   const size_t lds = sizeof(float) * (size_t)ch * per;
-  return launch_kernel(small_update_kernel, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2, ldd2,
-                       W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom);
+  if (limit > 0.f)
+    return launch_kernel(small_update_kernel<true>, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2,
+                         ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom, limit, faults);
+  return launch_kernel(small_update_kernel<false>, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2,
+                       ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom, limit, faults);
 }
 
 }  // namespace bpk

@@ -56,4 +56,12 @@ def test_null_net_is_rejected(bp):
     assert L.bp_train_batches_onehot(None, None, 7, None, 0, 1, 0.1, 0.9, None) == bp.BP_EINVAL
     assert L.bp_forward(None, None, 0, None) == bp.BP_EINVAL
     assert L.bp_forward_onehot(None, None, 7, 0, None) == bp.BP_EINVAL
+    assert L.bp_set_sigmoid(None, 1) == bp.BP_EINVAL
+    assert L.bp_set_fault_limit(None, 1.0) == bp.BP_EINVAL
+    assert L.bp_get_fault_count(None, None) == bp.BP_EINVAL
+    assert L.bp_checkpoint_save(None) == bp.BP_EINVAL
+    assert L.bp_checkpoint_restore(None) == bp.BP_EINVAL
+    assert L.bp_guard_config(None, 1, 2.0) == bp.BP_EINVAL
+    assert L.bp_guard_epoch(None, 1.0, None) == bp.BP_EINVAL
+    assert L.bp_profile(None, 1) == bp.BP_EINVAL
     L.bp_destroy(None)   # no-op

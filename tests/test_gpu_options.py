@@ -1,0 +1,261 @@
+"""GPU parity of the method's options against the CPU oracle.
+
+* Table sigmoid (section 4.3): forward outputs, one update and epoch errors
+  against the oracle's table sigmoid, through every kernel that evaluates the
+  nonlinearity (fused small-net path, one-hot gather, dense forward product,
+  output-layer product and its split-K finish).
+* Range check of summed changes (section 8): the fault count is an integer,
+  compared exactly, with the closed form and with the oracle, for a poisoned
+  target on every update kernel (fused small-net update, one-hot scatter,
+  dense change product, split-K finish, bias row); weights after the update
+  against the oracle; a generous limit leaves results bit-identical.
+  The decisions are never near the limit (NaN, 1e30 against 1e6; 1e-30 against
+  changes of order 1e-3 or exactly 0), so float and double agree on them.
+* Checkpoint and guard (section 10.4): save/restore round trip, and a run
+  with a transient corruption that the guard rolls back ends bit-identical to
+  a clean run, with the oracle's guard taking the same decisions.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1801_01554_amd import bp
+from paper_1801_01554_amd import workloads as wl
+from parity_util import SSE_TOL, W_TOL, rel, rel_maxabs, to_device
+
+pytestmark = pytest.mark.gpu
+FWD_TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU parity tests need a ROCm device"
+    bp.lib()
+    return torch.device("cuda:0")
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _pair(w, table=False, limit=None, storage=64):
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    o = oracle.OracleNet(w.sizes, storage)
+    o.set_weights(w.weights.astype(np.float64))
+    if table:
+        net.set_sigmoid(bp.BP_SIGMOID_TABLE)
+        o.set_sigmoid(oracle.OracleNet.SIGMOID_TABLE)
+    if limit is not None:
+        net.set_fault_limit(limit)
+        o.set_fault_limit(limit)
+    return net, o
+
+
+def _epoch(net, o, w, dev, batch, lr, mom, t=None):
+    x, a, td = to_device(w, dev)
+    tn = w.targets if t is None else t
+    if t is not None:
+        td = torch.from_numpy(t).to(dev)
+    if a is not None:
+        sg = net.train_batches(td, batch, lr, mom, active=a)
+        so = o.train_epoch(tn, batch, lr, mom, active=w.active)
+    else:
+        sg = net.train_batches(td, batch, lr, mom, inputs=x)
+        so = o.train_epoch(tn, batch, lr, mom, x=w.inputs)
+    return sg, so
+
+
+# --------------------------------------------------------------------------- table sigmoid
+@pytest.mark.parametrize("sizes,n,onehot", [((70, 45, 9), 300, False), ((64, 1100, 16), 256, False),
+                                            ((203, 120, 26), 700, True), ((203, 300, 26), 65, True),
+                                            ((33, 5, 7, 9, 2), 40, False)])
+def test_table_forward_matches_oracle(dev, sizes, n, onehot):
+    _say(f"case table forward sizes={sizes} n={n} onehot={onehot}")
+    w = wl.make_custom(sizes, n, seed=31 + n, onehot=onehot, input_kind="normal",
+                       init="uniform0.3" if onehot else "fanin")
+    net, o = _pair(w, table=True)
+    x, a, _ = to_device(w, dev)
+    y = (net.forward(active=a) if onehot else net.forward(inputs=x)).cpu().numpy()
+    ref = o.forward(active=w.active) if onehot else o.forward(x=w.inputs)
+    err = float(np.max(np.abs(y - ref)))
+    _say(f"  max abs err {err}")
+    assert err <= FWD_TOL
+    # and it is the table, not the exact logistic, that both evaluate
+    exact = oracle.OracleNet(sizes, 64)
+    exact.set_weights(w.weights.astype(np.float64))
+    ref_exact = exact.forward(active=w.active) if onehot else exact.forward(x=w.inputs)
+    assert np.max(np.abs(ref - ref_exact)) > 10 * err
+
+
+@pytest.mark.parametrize("sizes,n,batch,onehot", [((203, 120, 26), 512, 512, True),    # fused small-net path
+                                                  ((203, 300, 26), 300, 300, True),    # one-hot gather/scatter
+                                                  ((70, 45, 9), 300, 100, False),      # dense products
+                                                  ((64, 1100, 16), 256, 256, False)])  # split-K output layer
+def test_table_update_matches_oracle(dev, sizes, n, batch, onehot):
+    _say(f"case table update sizes={sizes} n={n} batch={batch}")
+    w = wl.make_custom(sizes, n, seed=41 + n, onehot=onehot, init="uniform0.3" if onehot else "fanin")
+    net, o = _pair(w, table=True)
+    sg, so = _epoch(net, o, w, dev, batch, 0.1, 0.9)
+    ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
+    _say(f"  weights rel err {ew}, sse {sg} vs {so}")
+    assert max(ew) <= W_TOL
+    assert rel(sg, so) <= SSE_TOL
+
+
+def test_table_epochs_match_oracle_nettalk(dev):
+    w = wl.make("nettalk-120-b512")
+    _say("case table epochs nettalk-120-b512")
+    net, o = _pair(w, table=True)
+    for e in range(3):
+        sg, so = _epoch(net, o, w, dev, w.batch, w.lr, w.momentum)
+        _say(f"  epoch {e}: sse gpu {sg} oracle {so}")
+        assert rel(sg, so) <= SSE_TOL
+
+
+# --------------------------------------------------------------------------- range check
+def _poison_case(sizes, n, onehot, seed):
+    return wl.make_custom(sizes, n, seed=seed, onehot=onehot, init="uniform0.3" if onehot else "fanin")
+
+
+# (sizes, n, batch, onehot, poison): every update kernel
+POISON_CASES = [
+    ((203, 120, 26), 64, 64, True, np.nan),        # fused small-net update
+    ((203, 300, 26), 96, 96, True, 1e30),          # one-hot scatter + dense output change
+    ((70, 45, 9), 200, 200, False, 1e30),          # dense change products (fused update epilogue)
+    ((40, 30, 20), 2048, 2048, False, np.nan),     # split-K change + bias rows
+    ((33, 20, 12, 5), 100, 100, False, 1e30),      # three layers
+]
+
+
+def _expected_faults(sizes, onehot, k_active=7):
+    # poisoned output k of one pattern: every summed change it reaches
+    #   output layer: column k (n_{L-1} + 1 entries)
+    #   hidden layers l >= 1: all of W_l (delta_{l+1} of that pattern is huge everywhere)
+    #   first layer: the rows of the pattern's nonzero inputs plus the bias row
+    L = len(sizes) - 1
+    c = sizes[L - 1] + 1
+    for l in range(1, L - 1):
+        c += (sizes[l] + 1) * sizes[l + 1]
+    if L >= 2:
+        c += ((k_active if onehot else sizes[0]) + 1) * sizes[1]
+    return c
+
+
+@pytest.mark.parametrize("sizes,n,batch,onehot,poison", POISON_CASES)
+def test_fault_count_poisoned_target(dev, sizes, n, batch, onehot, poison):
+    _say(f"case faults sizes={sizes} n={n} batch={batch} onehot={onehot} poison={poison}")
+    w = _poison_case(sizes, n, onehot, seed=51 + n)
+    t = w.targets.copy()
+    t[n // 3, sizes[-1] // 2] = poison
+    net, o = _pair(w, limit=1e6)
+    _epoch(net, o, w, dev, batch, 0.2, 0.9, t=t)
+    want = _expected_faults(sizes, onehot)
+    got = net.fault_count()
+    _say(f"  faults gpu {got} oracle {o.fault_count()} closed form {want}")
+    assert got == want == o.fault_count()
+    ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
+    ev = rel_maxabs(w.sizes, net.get_momentum(), o.get_momentum())
+    _say(f"  weights rel err {ew}, momentum {ev}")
+    assert max(ew) <= W_TOL
+    assert np.all(np.isfinite(net.get_weights()))
+
+
+def test_tiny_limit_faults_every_nonzero_change(dev):
+    # 8 patterns of the fused small-net path: rows of W0 no pattern activates
+    # have a summed change of exactly 0 (in range); everything else faults.
+    sizes = (203, 120, 26)
+    w = _poison_case(sizes, 8, True, seed=61)
+    net, o = _pair(w, limit=1e-30)
+    _epoch(net, o, w, dev, 8, 0.2, 0.9)
+    unused = sizes[0] - len(np.unique(w.active))
+    want = wl.num_weights(sizes) - unused * sizes[1]
+    _say(f"  faults gpu {net.fault_count()} oracle {o.fault_count()} closed form {want}")
+    assert net.fault_count() == want == o.fault_count()
+
+
+@pytest.mark.parametrize("sizes,n,batch,onehot", [((203, 120, 26), 1024, 256, True), ((40, 30, 20), 2048, 1024, False),
+                                                  ((70, 45, 9), 300, 100, False)])
+def test_generous_limit_is_bit_identical(dev, sizes, n, batch, onehot):
+    _say(f"case generous limit sizes={sizes}")
+    w = _poison_case(sizes, n, onehot, seed=71)
+    x, a, t = to_device(w, dev)
+    outs = []
+    for limit in (None, 1e30):
+        net = bp.Net(sizes)
+        net.set_weights(w.weights)
+        if limit is not None:
+            net.set_fault_limit(limit)
+        kw = {"active": a} if onehot else {"inputs": x}
+        sse = net.train_batches(t, batch, 0.2, 0.9, **kw)
+        outs.append((net.get_weights(), net.get_momentum(), sse, net.fault_count()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    assert outs[0][2] == outs[1][2] and outs[1][3] == 0
+
+
+# --------------------------------------------------------------------------- checkpoint and guard
+def test_checkpoint_roundtrip(dev):
+    w = _poison_case((70, 45, 9), 300, False, seed=81)
+    x, _, t = to_device(w, dev)
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    with pytest.raises(bp.BPError):
+        net.checkpoint_restore()                 # nothing saved yet
+    net.train_batches(t, 100, 0.2, 0.9, inputs=x)
+    w1, v1 = net.get_weights(), net.get_momentum()
+    net.checkpoint_save()
+    net.train_batches(t, 100, 0.2, 0.9, inputs=x)
+    assert not np.array_equal(net.get_weights(), w1)
+    net.checkpoint_restore()
+    np.testing.assert_array_equal(net.get_weights(), w1)
+    np.testing.assert_array_equal(net.get_momentum(), v1)
+
+
+def test_guard_rolls_back_transient_corruption(dev):
+    sizes = (60, 40, 10)
+    w = _poison_case(sizes, 240, False, seed=91)
+    x, _, t = to_device(w, dev)
+    args = dict(batch=60, lr=0.02, momentum=0.9, inputs=x)   # clean errors change by < 1% per epoch
+
+    clean = bp.Net(sizes)
+    clean.set_weights(w.weights)
+    sse_clean = [clean.train_batches(t, **args) for _ in range(6)]
+
+    net = bp.Net(sizes)
+    net.set_weights(w.weights)
+    net.guard_config(every=2, jump=1.5)
+    o = oracle.OracleNet(sizes, 64)
+    o.guard_config(every=2, jump=1.5)
+    accepted, decisions = [], []
+    while len(accepted) < 6:
+        if len(accepted) == 3 and not decisions.count(1):
+            bad = -50.0 * net.get_weights()     # a transient corruption: saturated, wrong-way units
+            v = net.get_momentum()
+            net.set_weights(bad)
+            net.set_momentum(v)
+        sse = net.train_batches(t, **args)
+        r = net.guard_epoch(sse)
+        assert r == o.guard_epoch(sse)           # the oracle's guard decides the same on the same errors
+        decisions.append(r)
+        if r:
+            accepted = accepted[: len(accepted) - (len(accepted) % 2)]
+            continue
+        accepted.append(sse)
+    _say(f"  decisions {decisions}")
+    assert decisions.count(1) == 1
+    assert accepted == sse_clean
+    np.testing.assert_array_equal(net.get_weights(), clean.get_weights())
+    np.testing.assert_array_equal(net.get_momentum(), clean.get_momentum())
+
+
+def test_option_arguments_are_checked(dev):
+    net = bp.Net((5, 3, 2))
+    for bad in (lambda: net.set_sigmoid(2), lambda: net.set_fault_limit(-1.0),
+                lambda: net.set_fault_limit(float("nan")), lambda: net.guard_epoch(1.0),
+                lambda: net.guard_config(0, 2.0), lambda: net.guard_config(1, 0.0)):
+        with pytest.raises(bp.BPError) as e:
+            bad()
+        assert e.value.code == bp.BP_EINVAL
+    assert net.fault_count() == 0
