@@ -61,6 +61,10 @@ def load():
         "orc_checkpoint_restore": (ctypes.c_int, [vp]),
         "orc_guard_config": (ctypes.c_int, [vp, ctypes.c_int32, ctypes.c_double]),
         "orc_guard_epoch": (ctypes.c_int, [vp, ctypes.c_double]),
+        "orc_set_context": (ctypes.c_int, [vp, ctypes.c_int32, _i32p, _i32p]),
+        "orc_train_sequences": (ctypes.c_int, [vp, _f32p, _f32p, _f32p, _f32p, ctypes.c_int64, ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_double, ctypes.c_double, _f64p, _f64p]),
+        "orc_forward_sequences": (ctypes.c_int, [vp, _f32p, _f32p, ctypes.c_int64, ctypes.c_int32, _f64p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -190,6 +194,37 @@ class OracleNet:
         if rc < 0:
             raise OracleError("guard_epoch: guard not configured")
         return rc
+
+    # recurrence (Elman nets, section 10.5) ---------------------------------
+    def set_context(self, from_layer, from_unit) -> None:
+        """Context unit c (input unit n_0 - n_ctx + c) copies unit from_unit[c] of hidden layer from_layer[c]."""
+        fl, fu = _i32(from_layer).reshape(-1), _i32(from_unit).reshape(-1)
+        if fl.size != fu.size:
+            raise OracleError("set_context: from_layer and from_unit differ in length")
+        self._chk(_lib.orc_set_context(self._h, fl.size, _p(fl, _i32p), _p(fu, _i32p)), "set_context")
+
+    def train_sequences(self, x, t, cont, mask, steps_per_update: int, lr: float, momentum: float,
+                        per_window: bool = False):
+        """Elman training over [n_steps][n_streams] patterns; returns the summed squared error."""
+        x, t, cont, mask = _f32(x), _f32(t), _f32(cont), _f32(mask)
+        T, S = cont.shape
+        nw = (T + steps_per_update - 1) // steps_per_update if steps_per_update > 0 else 0
+        wsse = np.zeros(max(nw, 1), np.float64)
+        sse = ctypes.c_double(0.0)
+        rc = _lib.orc_train_sequences(self._h, _p(x, _f32p), _p(t, _f32p), _p(cont, _f32p), _p(mask, _f32p), T, S,
+                                      int(steps_per_update), float(lr), float(momentum), ctypes.byref(sse),
+                                      _p(wsse, _f64p))
+        self._chk(rc, "train_sequences")
+        return (sse.value, wsse[:nw]) if per_window else sse.value
+
+    def forward_sequences(self, x, cont) -> np.ndarray:
+        """Outputs [n_steps][n_streams][n_L] of the sequences at the current weights."""
+        x, cont = _f32(x), _f32(cont)
+        T, S = cont.shape
+        y = np.empty((T, S, self.sizes[-1]), np.float64)
+        self._chk(_lib.orc_forward_sequences(self._h, _p(x, _f32p), _p(cont, _f32p), T, S, _p(y, _f64p)),
+                  "forward_sequences")
+        return y
 
     # method --------------------------------------------------------------
     def forward(self, x=None, active=None) -> np.ndarray:

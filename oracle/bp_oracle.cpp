@@ -59,6 +59,20 @@
  *   range check     each summed change G (the "total weight change" of section
  *             8) outside [-limit, limit], or not a number, is set to zero
  *             before the update and counted as a fault (section 8).
+ *   recurrence      Elman nets (section 10.5): the last n_ctx input units are
+ *             context units; before each pattern of a sequence, context unit
+ *             c receives a copy of unit ctx_unit[c] of hidden layer
+ *             ctx_layer[c] as it was after the previous pattern of the same
+ *             sequence, multiplied by the pattern's continuation flag (1 to
+ *             continue a sequence, 0 at a sequence start).  Sequences are
+ *             handled in parallel across streams: pattern (t, s) is step t
+ *             of stream s, and the error of every pattern is multiplied by
+ *             its mask flag (0 for the padding after a stream's last
+ *             sequence), so a masked pattern back-propagates nothing.  A
+ *             pooled update follows every `steps_per_update` steps (all
+ *             streams); context values are inputs to the change like any
+ *             other input (no propagation through time).  Context starts at
+ *             zero in every call.
  *   checkpoint      one stored copy of W and V (section 10.4), and a guard that
  *             saves it every `every` accepted epochs and restores it when an
  *             epoch's error exceeds `jump` times the last accepted epoch's
@@ -113,6 +127,7 @@ struct Net {
   int64_t faults = 0;
   std::vector<Real> ckW, ckV;   // checkpoint
   Guard guard;
+  std::vector<int> ctx_layer, ctx_unit;   // Elman context: source of context unit c
 
   const Real* w(int l) const { return W.data() + off[l]; }
   Real* w(int l) { return W.data() + off[l]; }
@@ -176,12 +191,12 @@ void forward_pattern(const Net<Real>& net, std::vector<Real*>& a, bool sparse0) 
 
 // Deltas of one pattern from its activations and target; returns sum e^2.
 template <typename Real>
-double backward_pattern(const Net<Real>& net, Real* const* a, Real* const* d, const float* t) {
+double backward_pattern(const Net<Real>& net, Real* const* a, Real* const* d, const float* t, double mask = 1.0) {
   const int L = net.L, nL = net.n[L];
   double sse = 0.0;
   for (int k = 0; k < nL; ++k) {
     const double y = (double)a[L][k];
-    const double e = (double)t[k] - y;
+    const double e = mask * ((double)t[k] - y);     // the error times the pattern's mask flag
     sse += e * e;
     d[L][k] = (Real)(e * y * (1.0 - y));
   }
@@ -377,6 +392,63 @@ int train_epoch(Net<Real>& net, const float* x, const int32_t* act, int n_active
     batch_sum(net, st, rows, G.data());
     apply_update(net, G.data(), lr, mom);
     if (batch_sse) batch_sse[b] = bs;
+    total += bs;
+  }
+  if (sse) *sse = total;
+  return 0;
+}
+
+// Elman training over n_steps x n_streams patterns (see the header comment).
+// x: [n_steps][n_streams][n_ext], t: [n_steps][n_streams][n_L],
+// cont, mask: [n_steps][n_streams]; window_sse receives each update's error.
+// With train == false only the forward passes run and y (if given) receives
+// the outputs [n_steps][n_streams][n_L].
+template <typename Real>
+int train_sequences(Net<Real>& net, const float* x, const float* t, const float* cont, const float* mask,
+                    int64_t n_steps, int n_streams, int steps_per_update, double lr, double mom, double* sse,
+                    double* window_sse, double* y, bool train) {
+  const int L = net.L, n0 = net.n[0], nL = net.n[L];
+  const int n_ctx = (int)net.ctx_layer.size(), n_ext = n0 - n_ctx;
+  if (n_steps < 0 || n_streams < 1 || steps_per_update < 1 || (n_steps > 0 && (!x || !cont))) return -1;
+  if (train && n_steps > 0 && (!t || !mask)) return -1;
+  if (n_ctx > 0 && L < 2) return -1;
+  const int S = n_streams;
+  std::vector<double> prev((size_t)S * n_ctx, 0.0);   // context sources after the previous step
+  const int64_t rows_max = (int64_t)std::min<int64_t>(steps_per_update, std::max<int64_t>(n_steps, 1)) * S;
+  BatchState<Real> st;
+  alloc_state(net, st, rows_max);
+  std::vector<double> G(train ? (size_t)net.total : 0);
+  double total = 0.0;
+  int64_t wi = 0;
+  for (int64_t w0 = 0; w0 < n_steps; w0 += steps_per_update, ++wi) {
+    const int steps = (int)std::min<int64_t>(steps_per_update, n_steps - w0);
+    for (int k = 0; k < steps; ++k) {
+      const int64_t g = w0 + k;
+#pragma omp parallel for schedule(static)
+      for (int s = 0; s < S; ++s) {
+        const int64_t p = (int64_t)k * S + s;            // row within the window
+        const int64_t q = g * S + s;                     // pattern (step g, stream s)
+        std::vector<Real*> a(L + 1), d(L + 1, nullptr);
+        for (int l = 0; l <= L; ++l) a[l] = st.a[l].data() + p * net.n[l];
+        for (int i = 0; i < n_ext; ++i) a[0][i] = (Real)x[q * n_ext + i];
+        for (int c = 0; c < n_ctx; ++c) a[0][n_ext + c] = (Real)((double)cont[q] * prev[(size_t)s * n_ctx + c]);
+        forward_pattern(net, a, false);
+        if (train) {
+          for (int l = 1; l <= L; ++l) d[l] = st.d[l].data() + p * net.n[l];
+          st.sse_p[p] = backward_pattern(net, a.data(), d.data(), t + q * nL, (double)mask[q]);
+        } else if (y) {
+          for (int j = 0; j < nL; ++j) y[q * nL + j] = (double)a[L][j];
+        }
+        for (int c = 0; c < n_ctx; ++c) prev[(size_t)s * n_ctx + c] = (double)a[net.ctx_layer[c]][net.ctx_unit[c]];
+      }
+    }
+    if (!train) continue;
+    const int64_t rows = (int64_t)steps * S;
+    double bs = 0.0;
+    for (int64_t p = 0; p < rows; ++p) bs += st.sse_p[p];
+    batch_sum(net, st, rows, G.data());
+    apply_update(net, G.data(), lr, mom);
+    if (window_sse) window_sse[wi] = bs;
     total += bs;
   }
   if (sse) *sse = total;
@@ -586,6 +658,45 @@ int orc_guard_config(orc_net* h, int32_t every, double jump) {
 int orc_guard_epoch(orc_net* h, double sse) {
   if (!h) return -1;
   auto f = [&](auto& net) { return net.guard.on ? guard_epoch(net, sse) : -1; };
+  return ORC_DISPATCH(h, f);
+}
+
+// Elman context (section 10.5): context unit c (input unit n_0 - n_ctx + c)
+// copies unit from_unit[c] of hidden layer from_layer[c] (1 <= layer <= L-1).
+// n_ctx == 0 removes the context.
+int orc_set_context(orc_net* h, int32_t n_ctx, const int32_t* from_layer, const int32_t* from_unit) {
+  if (!h || n_ctx < 0 || (n_ctx > 0 && (!from_layer || !from_unit))) return -1;
+  auto f = [&](auto& net) {
+    if (n_ctx > net.n[0] || (n_ctx > 0 && net.L < 2)) return -1;
+    for (int c = 0; c < n_ctx; ++c)
+      if (from_layer[c] < 1 || from_layer[c] > net.L - 1 || from_unit[c] < 0 || from_unit[c] >= net.n[from_layer[c]])
+        return -1;
+    net.ctx_layer.assign(from_layer, from_layer + n_ctx);
+    net.ctx_unit.assign(from_unit, from_unit + n_ctx);
+    return 0;
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+int orc_train_sequences(orc_net* h, const float* x, const float* t, const float* cont, const float* mask,
+                        int64_t n_steps, int32_t n_streams, int32_t steps_per_update, double lr, double mom,
+                        double* sse, double* window_sse) {
+  if (!h) return -1;
+  auto f = [&](auto& net) {
+    return train_sequences(net, x, t, cont, mask, n_steps, n_streams, steps_per_update, lr, mom, sse, window_sse,
+                           nullptr, true);
+  };
+  return ORC_DISPATCH(h, f);
+}
+
+// Outputs y [n_steps][n_streams][n_L] of the sequences at the current weights (no update).
+int orc_forward_sequences(orc_net* h, const float* x, const float* cont, int64_t n_steps, int32_t n_streams,
+                          double* y) {
+  if (!h || (n_steps > 0 && !y)) return -1;
+  auto f = [&](auto& net) {
+    return train_sequences(net, x, nullptr, cont, nullptr, n_steps, n_streams, 1, 0.0, 0.0, nullptr, nullptr, y,
+                           false);
+  };
   return ORC_DISPATCH(h, f);
 }
 

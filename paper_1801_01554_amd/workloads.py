@@ -196,3 +196,122 @@ def dense_from_active(active: np.ndarray, n0: int) -> np.ndarray:
         rows = np.repeat(np.arange(n), active.shape[1])
         x[rows, active.reshape(-1)] = 1.0
     return x
+
+
+# ---------------------------------------------------------------------------
+# Sequences for Elman nets (section 10.5).  The paper's speech data is not
+# available; these synthetic sequences stand in with its structure: frames
+# of features, a class per frame, sequences of mixed length packed into
+# parallel streams (one stream per processor in the paper), the padding
+# after a stream's last whole sequence marked by a zero mask flag.
+#
+# Recipe (streams 3, 4, 5 of the seed: sequence layout, frames, weights):
+#   * stream s is filled with sequences of length integers(len_min,
+#     len_max + 1) while the next one fits in n_steps; continuation flag 0 at
+#     each sequence start and 1 inside; steps after the last sequence get
+#     continuation 0 and mask 0, other steps mask 1;
+#   * a sequence is a run of segments of integers(3, 11) frames; each
+#     segment has a class uniform over the n_out classes; a frame's features
+#     are that class's embedding (standard normal, n_out x n_ext, one per
+#     workload) plus 0.5 standard normal noise;
+#   * targets: 0.9 for the frame's class, 0.1 for the others (padding frames
+#     draw a class too; their mask is 0);
+#   * weights uniform(-1/sqrt(fan_in), 1/sqrt(fan_in)) like the dense nets;
+#   * the context (n_ctx units, the last inputs) copies the first n_ctx
+#     units of hidden layer 1.
+
+@dataclasses.dataclass(frozen=True)
+class SeqSpec:
+    name: str
+    n_ext: int              # external inputs per frame
+    hidden: tuple           # hidden layer sizes
+    n_out: int              # classes = output units
+    n_ctx: int              # context units (copies of hidden layer 1)
+    n_streams: int
+    n_steps: int
+    steps_per_update: int
+    len_min: int
+    len_max: int
+    lr: float
+    momentum: float
+    epochs: int
+    seed: int
+    note: str = ""
+
+    @property
+    def sizes(self) -> tuple:
+        return (self.n_ext + self.n_ctx,) + tuple(self.hidden) + (self.n_out,)
+
+
+SEQ_SPECS = {
+    s.name: s
+    for s in [
+        SeqSpec("elman-64+256-256-64", 64, (256,), 64, 256, 1024, 128, 8, 16, 64, 5e-6, 0.9, 1, 6,
+                "Elman net, 1024 parallel streams of 16-64-frame sequences, an update every 8 steps"),
+        SeqSpec("elman-20+48-48-12", 20, (48,), 12, 48, 200, 37, 5, 4, 12, 5e-4, 0.9, 3, 7,
+                "small Elman net with a ragged stream count and a short last window"),
+    ]
+}
+
+
+@dataclasses.dataclass
+class SeqWorkload:
+    spec: SeqSpec
+    inputs: np.ndarray      # float32 [n_steps][n_streams][n_ext]
+    targets: np.ndarray     # float32 [n_steps][n_streams][n_out]
+    cont: np.ndarray        # float32 [n_steps][n_streams]: 1 continues a sequence, 0 starts one
+    mask: np.ndarray        # float32 [n_steps][n_streams]: 0 on the padding after a stream's last sequence
+    weights: np.ndarray     # float32 flat, C-ABI layout
+    ctx_layer: np.ndarray   # int32 [n_ctx]
+    ctx_unit: np.ndarray    # int32 [n_ctx]
+
+    @property
+    def sizes(self) -> tuple:
+        return self.spec.sizes
+
+    @property
+    def lr(self) -> float:
+        return float(np.float32(self.spec.lr))
+
+    @property
+    def momentum(self) -> float:
+        return float(np.float32(self.spec.momentum))
+
+    @property
+    def n_patterns(self) -> int:
+        return self.spec.n_steps * self.spec.n_streams
+
+
+def make_sequences(spec) -> SeqWorkload:
+    """Builds a sequence workload from a SeqSpec or the name of one."""
+    s = SEQ_SPECS[spec] if isinstance(spec, str) else spec
+    T, S = s.n_steps, s.n_streams
+    g_lay, g_frm = _rng(s.seed, 3), _rng(s.seed, 4)
+    cont = np.zeros((T, S), np.float32)
+    mask = np.zeros((T, S), np.float32)
+    cls = np.zeros((T, S), np.int64)
+    for st in range(S):
+        pos = 0
+        while True:
+            n = int(g_lay.integers(s.len_min, s.len_max + 1))
+            if pos + n > T:
+                break
+            cont[pos + 1:pos + n, st] = 1.0
+            mask[pos:pos + n, st] = 1.0
+            pos += n
+        # classes in segments over the whole stream (padding included)
+        t0 = 0
+        while t0 < T:
+            m = int(g_lay.integers(3, 11))
+            cls[t0:t0 + m, st] = g_lay.integers(0, s.n_out)
+            t0 += m
+    emb = g_frm.standard_normal((s.n_out, s.n_ext))
+    x = np.empty((T, S, s.n_ext), np.float32)
+    for t in range(T):
+        x[t] = emb[cls[t]] + 0.5 * g_frm.standard_normal((S, s.n_ext))
+    tg = np.full((T, S, s.n_out), 0.1, np.float32)
+    np.put_along_axis(tg, cls[:, :, None], np.float32(0.9), axis=2)
+    w = draw_weights(s.seed, s.sizes, "fanin")
+    ctx_layer = np.ones(s.n_ctx, np.int32)
+    ctx_unit = np.arange(s.n_ctx, dtype=np.int32)
+    return SeqWorkload(s, x, tg, cont, mask, w, ctx_layer, ctx_unit)

@@ -73,3 +73,28 @@ def test_custom_onehot_indices_distinct():
     w = wl.make_custom((50, 6, 3), 40, seed=2, onehot=True)
     for row in w.active:
         assert len(set(row.tolist())) == row.size
+
+
+# --------------------------------------------------------------------------- sequences
+@pytest.mark.parametrize("name", list(wl.SEQ_SPECS))
+def test_sequence_layout(name):
+    w = wl.make_sequences(name)
+    s = w.spec
+    T, S = s.n_steps, s.n_streams
+    assert w.inputs.shape == (T, S, s.n_ext) and w.targets.shape == (T, S, s.n_out)
+    assert w.cont.shape == w.mask.shape == (T, S)
+    assert w.weights.size == wl.num_weights(s.sizes)
+    for st in range(S):
+        m, c = w.mask[:, st], w.cont[:, st]
+        end = int(m.sum())
+        assert np.all(m[:end] == 1) and np.all(m[end:] == 0)          # padding only after the last sequence
+        assert np.all(c[end:] == 0) and (end == 0 or c[0] == 0)
+        starts = [0] + [t for t in range(1, end) if c[t] == 0] + [end]
+        lens = np.diff(starts)
+        assert np.all(lens >= s.len_min) and np.all(lens <= s.len_max)
+        assert T - end < s.len_max                                     # the next sequence did not fit
+    # one class per frame: exactly one 0.9 target
+    assert np.all(np.sum(w.targets == np.float32(0.9), axis=2) == 1)
+    w2 = wl.make_sequences(name)
+    np.testing.assert_array_equal(w.inputs, w2.inputs)
+    np.testing.assert_array_equal(w.cont, w2.cont)
