@@ -122,6 +122,46 @@ int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* 
 int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, int64_t n_patterns,
                       float* outputs_dev);
 
+/* ---- Elman nets (section 10.5: recurrent nets trained in parallel across
+ * sequences).
+ *
+ * Context units are the last n_ctx units of the input layer: context unit c
+ * (input unit n_0 - n_ctx + c) receives, before each pattern of a sequence,
+ * a copy of unit from_unit[c] of hidden layer from_layer[c] (1 <= layer <=
+ * min(L - 1, 8)) as it was after the previous pattern of the same sequence
+ * (the paper's list of (from unit, to unit) pairs).  The other n_0 - n_ctx
+ * inputs are the pattern's external inputs.  from_layer and from_unit are
+ * host arrays of n_ctx entries; n_ctx = 0 removes the context.  Waits for the
+ * net's stream. */
+int bp_set_context(bp_net* net, int32_t n_ctx, const int32_t* from_layer, const int32_t* from_unit);
+
+/* Trains on n_streams sequence streams of n_steps patterns each, pattern
+ * (t, s) being step t of stream s (the paper gives each processor its own
+ * sequences; here each stream is one).  Row-major device arrays:
+ *   inputs_dev  float [n_steps][n_streams][n_0 - n_ctx]  external inputs
+ *   targets_dev float [n_steps][n_streams][n_L]
+ *   cont_dev    float [n_steps][n_streams]  continuation flag: the copied
+ *               context is multiplied by it (1 continues the stream's
+ *               sequence, 0 starts a new one)
+ *   mask_dev    float [n_steps][n_streams]  the pattern's error is multiplied
+ *               by it (0 for the padding after a stream's last sequence, so
+ *               that it back-propagates nothing and adds no error)
+ * One pooled update (summed change, lr and momentum, as bp_train_batches)
+ * follows every steps_per_update steps of all streams, and one after the last
+ * step.  The context takes part in the change as an ordinary input (no
+ * propagation through time) and starts at zero in every call.  sse_out: the
+ * summed squared masked error, as bp_train_batches.  Returns BP_EINVAL for
+ * NULL pointers (n_steps > 0; inputs_dev may be NULL when n_0 == n_ctx),
+ * n_steps < 0, n_streams < 1 or steps_per_update < 1. */
+int bp_train_sequences(bp_net* net, const float* inputs_dev, const float* targets_dev, const float* cont_dev,
+                       const float* mask_dev, int64_t n_steps, int32_t n_streams, int32_t steps_per_update,
+                       float lr, float momentum, double* sse_out);
+
+/* Forward passes of sequences (no update): outputs_dev float
+ * [n_steps][n_streams][n_L]; inputs and flags as bp_train_sequences. */
+int bp_forward_sequences(bp_net* net, const float* inputs_dev, const float* cont_dev, int64_t n_steps,
+                         int32_t n_streams, float* outputs_dev);
+
 /* ---- Options of the method (all off after bp_create). */
 
 /* Unit nonlinearity (section 4.3).  BP_SIGMOID_EXACT: 1 / (1 + e^-x) in fp32
@@ -187,7 +227,8 @@ enum {
   BP_K_FUSED_FB = 9,  /* small one-hot nets: whole forward + backward pass  */
   BP_K_FUSED_UPD = 10,/* small one-hot nets: both layers' change + update   */
   BP_K_OUTFIN = 11,   /* split-K output layer: partial sums + deltas + error */
-  BP_K_COUNT = 12
+  BP_K_SEQ_IN = 12,   /* Elman nets: input rows of a step with the context copy */
+  BP_K_COUNT = 13
 };
 
 /* on != 0: from now on every kernel launch of this net is bracketed by HIP

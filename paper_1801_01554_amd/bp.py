@@ -24,12 +24,12 @@ LIB_PATH = os.path.join(HERE, "libbp.so")
 BP_OK, BP_EINVAL, BP_ENOMEM, BP_EDEVICE = 0, -1, -2, -3
 EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set_weights", "bp_get_weights",
            "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
-           "bp_forward_onehot", "bp_set_sigmoid", "bp_set_fault_limit", "bp_get_fault_count",
+           "bp_forward_onehot", "bp_set_context", "bp_train_sequences", "bp_forward_sequences", "bp_set_sigmoid", "bp_set_fault_limit", "bp_get_fault_count",
            "bp_checkpoint_save", "bp_checkpoint_restore", "bp_guard_config", "bp_guard_epoch", "bp_profile",
            "bp_profile_report", "bp_last_error")
 BP_SIGMOID_EXACT, BP_SIGMOID_TABLE = 0, 1
 KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce", "fused_fb",
-         "fused_update", "output_finish")
+         "fused_update", "output_finish", "seq_in")
 
 _lib = None
 _vp = ctypes.c_void_p
@@ -67,6 +67,10 @@ def lib():
                                                    ctypes.c_float, ctypes.c_float, _f64p]),
         "bp_forward": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, _vp]),
         "bp_forward_onehot": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, ctypes.c_int64, _vp]),
+        "bp_set_context": (ctypes.c_int, [_vp, ctypes.c_int32, _i32p, _i32p]),
+        "bp_train_sequences": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int32,
+                                              ctypes.c_int32, ctypes.c_float, ctypes.c_float, _f64p]),
+        "bp_forward_sequences": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int64, ctypes.c_int32, _vp]),
         "bp_set_sigmoid": (ctypes.c_int, [_vp, ctypes.c_int32]),
         "bp_set_fault_limit": (ctypes.c_int, [_vp, ctypes.c_float]),
         "bp_get_fault_count": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64)]),
@@ -141,6 +145,26 @@ def bp_forward(h, inputs_ptr: int, n: int, outputs_ptr: int) -> int:
 
 def bp_forward_onehot(h, active_ptr: int, n_active: int, n: int, outputs_ptr: int) -> int:
     return lib().bp_forward_onehot(h, _vp(active_ptr), n_active, n, _vp(outputs_ptr))
+
+
+def bp_set_context(h, from_layer, from_unit) -> int:
+    fl = np.ascontiguousarray(from_layer, dtype=np.int32).reshape(-1)
+    fu = np.ascontiguousarray(from_unit, dtype=np.int32).reshape(-1)
+    if fl.size != fu.size:
+        return BP_EINVAL
+    return lib().bp_set_context(h, fl.size, fl.ctypes.data_as(_i32p), fu.ctypes.data_as(_i32p))
+
+
+def bp_train_sequences(h, inputs_ptr: int, targets_ptr: int, cont_ptr: int, mask_ptr: int, n_steps: int,
+                       n_streams: int, steps_per_update: int, lr: float, momentum: float,
+                       sse: Optional[ctypes.c_double]) -> int:
+    return lib().bp_train_sequences(h, _vp(inputs_ptr), _vp(targets_ptr), _vp(cont_ptr), _vp(mask_ptr), n_steps,
+                                    n_streams, steps_per_update, lr, momentum,
+                                    ctypes.byref(sse) if sse is not None else None)
+
+
+def bp_forward_sequences(h, inputs_ptr: int, cont_ptr: int, n_steps: int, n_streams: int, outputs_ptr: int) -> int:
+    return lib().bp_forward_sequences(h, _vp(inputs_ptr), _vp(cont_ptr), n_steps, n_streams, _vp(outputs_ptr))
 
 
 def bp_set_sigmoid(h, mode: int) -> int:
@@ -267,6 +291,33 @@ class Net:
             rc = bp_train_batches(self._h, xp, tp, n, int(batch), float(lr), float(momentum), sse)
         self._chk(rc)
         return sse.value if want_sse else None
+
+    def set_context(self, from_layer, from_unit) -> None:
+        self._chk(bp_set_context(self._h, from_layer, from_unit))
+        self.n_ctx = int(np.asarray(from_layer).size)
+
+    def train_sequences(self, inputs, targets, cont, mask, steps_per_update: int, lr: float, momentum: float,
+                        want_sse: bool = True) -> Optional[float]:
+        """inputs [T][S][n_0 - n_ctx], targets [T][S][n_L], cont and mask [T][S]: device float tensors."""
+        T, S = int(cont.shape[0]), int(cont.shape[1])
+        n_ext = self.sizes[0] - getattr(self, "n_ctx", 0)
+        xp = _dev_ptr(inputs, torch.float32, (T, S, n_ext), "inputs")
+        tp = _dev_ptr(targets, torch.float32, (T, S, self.sizes[-1]), "targets")
+        cp = _dev_ptr(cont, torch.float32, (T, S), "cont")
+        mp = _dev_ptr(mask, torch.float32, (T, S), "mask")
+        sse = ctypes.c_double(0.0) if want_sse else None
+        self._chk(bp_train_sequences(self._h, xp, tp, cp, mp, T, S, int(steps_per_update), float(lr),
+                                     float(momentum), sse))
+        return sse.value if want_sse else None
+
+    def forward_sequences(self, inputs, cont) -> "torch.Tensor":
+        T, S = int(cont.shape[0]), int(cont.shape[1])
+        n_ext = self.sizes[0] - getattr(self, "n_ctx", 0)
+        xp = _dev_ptr(inputs, torch.float32, (T, S, n_ext), "inputs")
+        cp = _dev_ptr(cont, torch.float32, (T, S), "cont")
+        out = torch.empty((T, S, self.sizes[-1]), dtype=torch.float32, device=cont.device)
+        self._chk(bp_forward_sequences(self._h, xp, cp, T, S, out.data_ptr()))
+        return out
 
     def set_sigmoid(self, mode: int) -> None:
         self._chk(bp_set_sigmoid(self._h, mode))

@@ -20,7 +20,7 @@ OUT = os.path.join(HERE, "libbp.so")
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-SOURCES = ["bp_kernels.hip", "bp_small.hip", "bp_net.cpp"]
+SOURCES = ["bp_kernels.hip", "bp_small.hip", "bp_seq.hip", "bp_net.cpp"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]

@@ -50,7 +50,8 @@ int colsum_rows(int M);
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
                          int K, const float* bias, float* out, int ldo, const float* tab);
 
-// Output layer during training: y = sigma(A W + bias); e = T - y;
+// Output layer during training: y = sigma(A W + bias); e = (T - y) * mask[m]
+// (mask == nullptr: no mask);
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of
 // block b (b < output_delta_blocks(M, N, K)); colsum[t][n] = sum of delta
 // over rows [128 t, 128 t + 128) (t < colsum_rows(M)).  With
@@ -61,9 +62,11 @@ int output_delta_splits(int M, int N, int K);
 size_t output_delta_workspace(int M, int N, int K);
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M,
                                 int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                                int ldd, double* sse_part, float* colsum, int ldcs, float* ws, const float* tab);
+                                int ldd, double* sse_part, float* colsum, int ldcs, float* ws, const float* tab,
+                                const float* mask);
 hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab);
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab,
+                         const float* mask);
 
 // Hidden deltas: out[m][n] = (sum_k D[m][k] W[n][k]) * act[m][n] (1 - act[m][n]),
 // with W rows n < N the non-bias rows of the layer above (ldw floats apart);
@@ -132,6 +135,24 @@ hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int row
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
                         int lda1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
                         float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults);
+
+// ---- Elman nets (bp_seq.hip, section 10.5)
+// Hidden layers a context unit may copy from: 1 .. kCtxMaxLayer.
+constexpr int kCtxMaxLayer = 8;
+
+// Rows of the previous step's activations, per hidden layer (base[l] ==
+// nullptr: no previous step, the context is 0 times the flag).
+struct CtxSource {
+  const float* base[kCtxMaxLayer + 1];
+  int ld[kCtxMaxLayer + 1];
+};
+
+// Input rows of one step for S streams: A0[s][0 .. n_ext) = X[s][..];
+// A0[s][n_ext + c] = cont[s] * src.base[layer[c]][s * ld + unit[c]];
+// A0[s][n0 .. lda0) = 0.
+hipError_t seq_assemble(hipStream_t s, const float* X, int n_ext, const float* cont, int S, int n_ctx,
+                        const int32_t* ctx_layer, const int32_t* ctx_unit, const CtxSource& src, float* A0,
+                        int lda0);
 
 // out[0] = sum of part[0 .. n-1] in a fixed order (double).
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out);

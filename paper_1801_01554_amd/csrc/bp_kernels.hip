@@ -61,13 +61,15 @@ struct EpiOutputDelta {
   float* colsum;
   int ldcs;
   const float* tab;
+  const float* mask;     // per-row error multiplier (section 10.5), or nullptr
   static constexpr bool kSSE = true;
   static constexpr bool kColSum = true;
   static constexpr bool kFaults = false;
   __device__ float column(int n) const { return bias[n]; }
   __device__ float apply(int m, int n, float acc, float b, float& sse) const {
     const float y = unit_sigma(acc + b, tab);
-    const float e = T[(size_t)m * ldt + n] - y;
+    float e = T[(size_t)m * ldt + n] - y;
+    if (mask) e *= mask[m];
     sse += e * e;
     const float d = e * y * (1.0f - y);
     delta[(size_t)m * ldd + n] = d;
@@ -467,7 +469,8 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
                                                              int ldp, int M, int N, const float* __restrict__ bias,
                                                              const float* __restrict__ T, int ldt, float* delta,
                                                              int ldd, double* sse_part, float* colsum, int ldcs,
-                                                             const float* __restrict__ tab) {
+                                                             const float* __restrict__ tab,
+                                                             const float* __restrict__ mask) {
   constexpr int W = kFin / 64, R = 128 / W;
   __shared__ float cs[W][64];
   __shared__ float red[W];
@@ -494,7 +497,8 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
     for (int r = 0; r < R; ++r) {
       if (m0 + r >= M) break;
       const float y = unit_sigma(z[r] + b, tab);
-      const float e = t[r] - y;
+      float e = t[r] - y;
+      if (mask) e *= mask[m0 + r];
       sse += e * e;
       const float d = e * y * (1.0f - y);
       delta[(size_t)(m0 + r) * ldd + n] = d;
@@ -722,10 +726,10 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
 
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
                                 const float* bias, const float* T, int ldt, float* delta, int ldd, double* sse_part,
-                                float* colsum, int ldcs, float* ws, const float* tab) {
+                                float* colsum, int ldcs, float* ws, const float* tab, const float* mask) {
   const int sp = choose_output_splits(M, N, K);
   if (sp <= 1) {
-    EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs, tab};
+    EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs, tab, mask};
     return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
@@ -734,13 +738,14 @@ hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const fl
 }
 
 hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, const float* T, int ldt, float* delta,
-                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab) {
+                         int ldd, double* sse_part, float* colsum, int ldcs, const float* ws, const float* tab,
+                         const float* mask) {
   const int sp = choose_output_splits(M, N, K);
   if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
   const int ldp = (N + 3) / 4 * 4;
   dim3 grid((M + 127) / 128, (N + 63) / 64);
   return launch_kernel(output_finish_kernel, grid, kFin, 0, s, ws, sp, (size_t)M * ldp, ldp, M, N, bias, T, ldt,
-                       delta, ldd, sse_part, colsum, ldcs, tab);
+                       delta, ldd, sse_part, colsum, ldcs, tab, mask);
 }
 
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,

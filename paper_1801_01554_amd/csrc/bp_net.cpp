@@ -34,6 +34,7 @@ struct bp_net {
   int device = 0;
   // workspace
   int64_t ws_rows = 0;
+  int64_t ws_csum_top = 0;            // rows of csum[L] (per-step tiling of sequence windows)
   std::vector<float*> act;            // act[l], l = 1 .. L-1 : [ws_rows][lda[l]]
   std::vector<float*> del;            // del[l], l = 1 .. L   : [ws_rows][lda[l]]
   std::vector<float*> csum;           // csum[l], l = 1 .. L  : [colsum_rows(ws_rows)][lda[l]]
@@ -53,6 +54,13 @@ struct bp_net {
   // checkpoint of W and V (section 10.4) and the guard that uses it
   float* ckW = nullptr;
   float* ckV = nullptr;
+  // Elman context (section 10.5): context unit c (input n0 - n_ctx + c)
+  // copies unit ctx_unit[c] of hidden layer ctx_layer[c]
+  int n_ctx = 0;
+  int32_t* ctx_layer_dev = nullptr;
+  int32_t* ctx_unit_dev = nullptr;
+  float* seq_in = nullptr;            // assembled input rows of a window [rows][lda[0]]
+  size_t seq_in_cap = 0;
   struct Guard {
     bool on = false;
     int every = 1;
@@ -149,28 +157,45 @@ void free_workspace(bp_net* net) {
   net->del.assign(net->L + 1, nullptr);
   net->csum.assign(net->L + 1, nullptr);
   net->ws_rows = 0;
+  net->ws_csum_top = 0;
   free_ptr(net->splitk);
   net->splitk = nullptr;
   net->splitk_cap = 0;
 }
 
-int ensure_workspace(bp_net* net, int64_t rows) {
-  if (rows <= net->ws_rows) return BP_OK;
+// Floats of split-K workspace one forward pass over `fwd_rows` patterns and
+// the change products over `chg_rows` patterns need (used one at a time).
+// The output layer's need is not monotonic in its row count (fewer rows,
+// more splits), so callers ask for every row count they will use.
+size_t splitk_floats(const bp_net* net, int64_t fwd_rows, int64_t chg_rows) {
+  size_t sk = fwd_rows > 0 ? bpk::output_delta_workspace((int)fwd_rows, net->n[net->L], net->n[net->L - 1]) : 0;
+  for (int l = 0; l < net->L && chg_rows > 0; ++l)
+    sk = std::max(sk, bpk::change_update_workspace(net->n[l], net->n[l + 1], (int)chg_rows));
+  return sk;
+}
+
+// Workspace for batches of up to `rows` patterns, `top_csum` column-sum rows
+// of the output deltas (sequence windows tile them per step) and `splitk`
+// floats of split-K partials.  Grows only.
+int ensure_workspace(bp_net* net, int64_t rows, int64_t top_csum, size_t splitk) {
+  top_csum = std::max<int64_t>(top_csum, bpk::colsum_rows((int)rows));
+  if (rows <= net->ws_rows && top_csum <= net->ws_csum_top && splitk <= net->splitk_cap) return BP_OK;
+  rows = std::max(rows, net->ws_rows);
+  top_csum = std::max(top_csum, net->ws_csum_top);
+  splitk = std::max(splitk, net->splitk_cap);
   BP_HIP(net, hipStreamSynchronize(net->stream));
   free_workspace(net);
   for (int l = 1; l <= net->L; ++l) {
     const size_t bytes = sizeof(float) * (size_t)rows * net->lda[l];
     if (l < net->L) BP_HIP(net, hipMalloc(&net->act[l], bytes));
     BP_HIP(net, hipMalloc(&net->del[l], bytes));
-    BP_HIP(net, hipMalloc(&net->csum[l], sizeof(float) * (size_t)bpk::colsum_rows((int)rows) * net->lda[l]));
+    const int64_t cr = l == net->L ? top_csum : bpk::colsum_rows((int)rows);
+    BP_HIP(net, hipMalloc(&net->csum[l], sizeof(float) * (size_t)cr * net->lda[l]));
   }
-  // split-K partials: the output layer's and every change product's (used one at a time)
-  size_t sk = bpk::output_delta_workspace((int)rows, net->n[net->L], net->n[net->L - 1]);
-  for (int l = 0; l < net->L; ++l)
-    sk = std::max(sk, bpk::change_update_workspace(net->n[l], net->n[l + 1], (int)rows));
-  if (sk) BP_HIP(net, hipMalloc(&net->splitk, sizeof(float) * sk));
-  net->splitk_cap = sk;
+  if (splitk) BP_HIP(net, hipMalloc(&net->splitk, sizeof(float) * splitk));
+  net->splitk_cap = splitk;
   net->ws_rows = rows;
+  net->ws_csum_top = top_csum;
   return BP_OK;
 }
 
@@ -211,20 +236,33 @@ int copy_layers(bp_net* net, float* dev, const float* host_src, float* host_dst)
 
 // Inputs of one batch: dense rows or one-hot index rows.
 struct BatchInput {
-  const float* x = nullptr;       // dense [rows][n0]
+  const float* x = nullptr;       // dense [rows][ldx]
+  int ldx = 0;                    // row stride of x (0: n0)
   const int32_t* act = nullptr;   // one-hot [rows][n_active]
   int n_active = 0;
+};
+
+int ldx_of(const bp_net* net, const BatchInput& in) { return in.ldx > 0 ? in.ldx : net->n[0]; }
+
+// Where a training forward pass writes its output layer: deltas, their
+// per-tile column sums, and the optional per-pattern error mask.
+struct OutputView {
+  float* delta = nullptr;
+  float* csum = nullptr;
+  const float* mask = nullptr;
 };
 
 // Forward pass of `rows` patterns; the last layer either applies the output
 // delta epilogue (training, T != nullptr) or writes sigma to `out`.
 int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part,
-                float* out, int ldo, float* const* acts) {
+                float* out, int ldo, float* const* acts, OutputView ov = OutputView()) {
+  if (!ov.delta) ov.delta = net->del[net->L];
+  if (!ov.csum) ov.csum = net->csum[net->L];
   const int L = net->L;
   hipStream_t s = net->stream;
   for (int l = 0; l < L; ++l) {
     const bool last = (l == L - 1);
-    float* dst = last ? (T ? net->del[L] : out) : acts[l + 1];
+    float* dst = last ? (T ? ov.delta : out) : acts[l + 1];
     const int ldd = last ? (T ? net->lda[L] : ldo) : net->lda[l + 1];
     if (l == 0 && in.act) {
       BP_LAUNCH(net, BP_K_GATHER,
@@ -233,16 +271,16 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
       continue;
     }
     const float* A = (l == 0) ? in.x : acts[l];
-    const int ldA = (l == 0) ? net->n[0] : net->lda[l];
+    const int ldA = (l == 0) ? ldx_of(net, in) : net->lda[l];
     if (last && T) {
       BP_LAUNCH(net, BP_K_OUTPUT,
                 bpk::forward_output_delta(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
-                                          wbias(net, l), T, net->n[L], dst, ldd, sse_part, net->csum[L],
-                                          net->lda[L], net->splitk, net->sig_tab));
+                                          wbias(net, l), T, net->n[L], dst, ldd, sse_part, ov.csum,
+                                          net->lda[L], net->splitk, net->sig_tab, ov.mask));
       if (bpk::output_delta_splits(rows, net->n[l + 1], net->n[l]) > 1)
         BP_LAUNCH(net, BP_K_OUTFIN,
                   bpk::output_finish(s, rows, net->n[l + 1], net->n[l], wbias(net, l), T, net->n[L], dst, ldd,
-                                     sse_part, net->csum[L], net->lda[L], net->splitk, net->sig_tab));
+                                     sse_part, ov.csum, net->lda[L], net->splitk, net->sig_tab, ov.mask));
     } else
       BP_LAUNCH(net, BP_K_FORWARD,
                 bpk::forward_layer(s, A, ldA, wl(net, l), net->ldw[l], rows, net->n[l + 1], net->n[l],
@@ -279,7 +317,7 @@ int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, doubl
 
 // Backward pass and update of one batch whose deltas of the output layer are
 // in del[L].
-int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, float mom) {
+int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, float mom, int top_csum = 0) {
   hipStream_t s = net->stream;
   for (int l = net->L - 1; l >= 0; --l) {
     // Hidden deltas of layer l use W_l before its update.
@@ -295,7 +333,7 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
       continue;
     }
     const float* A = (l == 0) ? in.x : net->act[l];
-    const int ldA = (l == 0) ? net->n[0] : net->lda[l];
+    const int ldA = (l == 0) ? ldx_of(net, in) : net->lda[l];
     BP_LAUNCH(net, BP_K_CHANGE,
               bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
                                  wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk, net->fault_limit,
@@ -305,7 +343,8 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
                 bpk::splitk_finish(s, net->n[l], net->n[l + 1], rows, wl(net, l), vl(net, l), net->ldw[l], lr, mom,
                                    net->splitk, net->fault_limit, net->faults));
     BP_LAUNCH(net, BP_K_BIAS,
-              bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1], bpk::colsum_rows(rows), net->n[l + 1],
+              bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1],
+                               (l + 1 == net->L && top_csum > 0) ? top_csum : bpk::colsum_rows(rows), net->n[l + 1],
                                wbias(net, l), vbias(net, l), lr, mom, net->fault_limit, net->faults));
   }
   return BP_OK;
@@ -318,11 +357,13 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
     return BP_OK;
   }
   const int64_t rows_max = std::min<int64_t>(batch, n);
-  int rc = ensure_workspace(net, rows_max);
-  if (rc) return rc;
-  // exact number of error partials: every batch but the last has rows_max rows
+  // every batch but the last has rows_max rows
   const int64_t nb = (n + batch - 1) / batch;
   const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
+  int rc = ensure_workspace(net, rows_max, 0,
+                            std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows)));
+  if (rc) return rc;
+  // exact number of error partials
   const size_t need = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +
                       (size_t)sse_blocks(net, in, last_rows);
   rc = ensure_sse(net, need);
@@ -350,6 +391,121 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
   if (sse_out) {
     BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, net->stream));
     BP_HIP(net, hipStreamSynchronize(net->stream));
+  }
+  return BP_OK;
+}
+
+// ---- Elman nets (section 10.5)
+
+// Activation rows of `step` (S rows each) in the window buffers, per hidden
+// layer, as the context source of the next step.
+bpk::CtxSource ctx_source(bp_net* net, int64_t step, int S) {
+  bpk::CtxSource src{};
+  for (int l = 1; l < net->L && l <= bpk::kCtxMaxLayer; ++l) {
+    src.base[l] = step < 0 ? nullptr : net->act[l] + (size_t)step * S * net->lda[l];
+    src.ld[l] = net->lda[l];
+  }
+  return src;
+}
+
+int ensure_seq_in(bp_net* net, int64_t rows) {
+  const size_t need = (size_t)rows * net->lda[0];
+  if (need <= net->seq_in_cap) return BP_OK;
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  free_ptr(net->seq_in);
+  net->seq_in = nullptr;
+  net->seq_in_cap = 0;
+  BP_HIP(net, hipMalloc(&net->seq_in, sizeof(float) * need));
+  net->seq_in_cap = need;
+  return BP_OK;
+}
+
+// Training over n_steps x S patterns: windows of B steps; within a window,
+// step by step: assemble the input rows (external inputs, flag x context),
+// forward pass with masked output deltas; then one backward pass and pooled
+// update over all rows of the window.  Rows of a window are step-major.
+int train_sequences(bp_net* net, const float* X, const float* targets, const float* cont, const float* mask,
+                    int64_t T, int S, int B, float lr, float mom, double* sse_out) {
+  if (T == 0) {
+    if (sse_out) *sse_out = 0.0;
+    return BP_OK;
+  }
+  const int L = net->L, n_ext = net->n[0] - net->n_ctx, nL = net->n[L];
+  const int steps_max = (int)std::min<int64_t>(B, T);
+  const int last_steps = (int)(T - (T - 1) / B * B);
+  const int64_t rows_max = (int64_t)steps_max * S;
+  const int csS = bpk::colsum_rows(S);
+  int rc = ensure_workspace(net, rows_max, (int64_t)steps_max * csS,
+                            std::max({splitk_floats(net, S, rows_max), splitk_floats(net, 0, (int64_t)last_steps * S)}));
+  if (rc) return rc;
+  rc = ensure_seq_in(net, rows_max);
+  if (rc) return rc;
+  const int per_step = bpk::output_delta_blocks(S, nL, net->n[L - 1]);
+  rc = ensure_sse(net, (size_t)T * per_step);
+  if (rc) return rc;
+  hipStream_t s = net->stream;
+  std::vector<float*> acts(L + 1, nullptr);
+  size_t used = 0;
+  for (int64_t w0 = 0; w0 < T; w0 += B) {
+    const int steps = (int)std::min<int64_t>(B, T - w0);
+    for (int k = 0; k < steps; ++k) {
+      const int64_t g = w0 + k;
+      // context source: the previous step of this window, or the last step of
+      // the previous (full) window, or none at the first step of the call
+      const int64_t prev = k > 0 ? k - 1 : (w0 > 0 ? B - 1 : -1);
+      float* A0 = net->seq_in + (size_t)k * S * net->lda[0];
+      BP_LAUNCH(net, BP_K_SEQ_IN,
+                bpk::seq_assemble(s, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
+                                  net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, prev, S), A0, net->lda[0]));
+      BatchInput in;
+      in.x = A0;
+      in.ldx = net->lda[0];
+      for (int l = 1; l < L; ++l) acts[l] = net->act[l] + (size_t)k * S * net->lda[l];
+      OutputView ov;
+      ov.delta = net->del[L] + (size_t)k * S * net->lda[L];
+      ov.csum = net->csum[L] + (size_t)k * csS * net->lda[L];
+      ov.mask = mask + (size_t)g * S;
+      rc = run_forward(net, in, S, targets + (size_t)g * S * nL, net->sse_part + used, nullptr, 0, acts.data(), ov);
+      if (rc) return rc;
+      used += (size_t)per_step;
+    }
+    BatchInput win;
+    win.x = net->seq_in;
+    win.ldx = net->lda[0];
+    rc = run_backward_update(net, win, steps * S, lr, mom, steps * csS);
+    if (rc) return rc;
+  }
+  BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(s, net->sse_part, (int)used, net->sse_dev));
+  if (sse_out) {
+    BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, s));
+    BP_HIP(net, hipStreamSynchronize(s));
+  }
+  return BP_OK;
+}
+
+// Forward passes of the sequences (no update): hidden activations ping-pong
+// between two S-row halves of the workspace, the previous step's half being
+// the context source.
+int forward_sequences(bp_net* net, const float* X, const float* cont, int64_t T, int S, float* out) {
+  if (T == 0) return BP_OK;
+  const int L = net->L, n_ext = net->n[0] - net->n_ctx, nL = net->n[L];
+  int rc = ensure_workspace(net, 2 * (int64_t)S, 0, 0);
+  if (rc) return rc;
+  rc = ensure_seq_in(net, S);
+  if (rc) return rc;
+  std::vector<float*> acts(L + 1, nullptr);
+  for (int64_t g = 0; g < T; ++g) {
+    const int64_t half = g & 1;
+    BP_LAUNCH(net, BP_K_SEQ_IN,
+              bpk::seq_assemble(net->stream, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
+                                net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, g > 0 ? 1 - half : -1, S),
+                                net->seq_in, net->lda[0]));
+    BatchInput in;
+    in.x = net->seq_in;
+    in.ldx = net->lda[0];
+    for (int l = 1; l < L; ++l) acts[l] = net->act[l] + (size_t)half * S * net->lda[l];
+    rc = run_forward(net, in, S, nullptr, nullptr, out + (size_t)g * S * nL, nL, acts.data());
+    if (rc) return rc;
   }
   return BP_OK;
 }
@@ -470,6 +626,9 @@ void bp_destroy(bp_net* net) {
   free_ptr(net->faults);
   free_ptr(net->ckW);
   free_ptr(net->ckV);
+  free_ptr(net->ctx_layer_dev);
+  free_ptr(net->ctx_unit_dev);
+  free_ptr(net->seq_in);
   free_ptr(net->W);
   free_ptr(net->V);
   for (auto& r : net->recs) {
@@ -617,6 +776,65 @@ int bp_profile_report(bp_net* net, int64_t* launches, double* ms, int32_t n_kind
     ms[k] = net->prof_ms[k];
   }
   return BP_OK;
+}
+
+int bp_set_context(bp_net* net, int32_t n_ctx, const int32_t* from_layer, const int32_t* from_unit) {
+  if (check_net(net)) return BP_EINVAL;
+  if (n_ctx < 0 || n_ctx > net->n[0]) return fail(net, BP_EINVAL, "bp_set_context: n_ctx must be in [0, n_0]");
+  if (n_ctx > 0 && (!from_layer || !from_unit)) return fail(net, BP_EINVAL, "bp_set_context: NULL source arrays");
+  if (n_ctx > 0 && net->L < 2) return fail(net, BP_EINVAL, "bp_set_context: the net has no hidden layer");
+  for (int c = 0; c < n_ctx; ++c) {
+    const int l = from_layer[c];
+    if (l < 1 || l > net->L - 1 || l > bpk::kCtxMaxLayer || from_unit[c] < 0 || from_unit[c] >= net->n[l])
+      return fail(net, BP_EINVAL, "bp_set_context: a source is not a hidden unit (layers 1 .. min(L-1, 8))");
+  }
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  free_ptr(net->ctx_layer_dev);
+  free_ptr(net->ctx_unit_dev);
+  net->ctx_layer_dev = net->ctx_unit_dev = nullptr;
+  net->n_ctx = 0;
+  if (n_ctx > 0) {
+    BP_HIP(net, hipMalloc(&net->ctx_layer_dev, sizeof(int32_t) * n_ctx));
+    BP_HIP(net, hipMalloc(&net->ctx_unit_dev, sizeof(int32_t) * n_ctx));
+    BP_HIP(net, hipMemcpy(net->ctx_layer_dev, from_layer, sizeof(int32_t) * n_ctx, hipMemcpyHostToDevice));
+    BP_HIP(net, hipMemcpy(net->ctx_unit_dev, from_unit, sizeof(int32_t) * n_ctx, hipMemcpyHostToDevice));
+  }
+  net->n_ctx = n_ctx;
+  return BP_OK;
+}
+
+static int check_seq(bp_net* net, const void* X, const void* cont, int64_t T, int32_t S, const char* who) {
+  std::string w(who);
+  if (T < 0 || S < 1) return fail(net, BP_EINVAL, w + ": need n_steps >= 0 and n_streams >= 1");
+  if (T * (int64_t)S > ((int64_t)1 << 31) - 1) return fail(net, BP_EINVAL, w + ": too many patterns");
+  if (T > 0 && (!cont || (!X && net->n[0] > net->n_ctx))) return fail(net, BP_EINVAL, w + ": NULL pointer");
+  if (T > 0 && (!aligned_ptr(X, 4) || !aligned_ptr(cont, 4)))
+    return fail(net, BP_EINVAL, w + ": pointers must be 4-byte aligned");
+  return BP_OK;
+}
+
+int bp_train_sequences(bp_net* net, const float* inputs_dev, const float* targets_dev, const float* cont_dev,
+                       const float* mask_dev, int64_t n_steps, int32_t n_streams, int32_t steps_per_update, float lr,
+                       float momentum, double* sse_out) {
+  if (check_net(net)) return BP_EINVAL;
+  int rc = check_seq(net, inputs_dev, cont_dev, n_steps, n_streams, "bp_train_sequences");
+  if (rc) return rc;
+  if (steps_per_update < 1) return fail(net, BP_EINVAL, "bp_train_sequences: steps_per_update < 1");
+  if ((int64_t)steps_per_update * n_streams > ((int64_t)1 << 30))
+    return fail(net, BP_EINVAL, "bp_train_sequences: steps_per_update x n_streams too large");
+  if (n_steps > 0 && (!targets_dev || !mask_dev || !aligned_ptr(targets_dev, 4) || !aligned_ptr(mask_dev, 4)))
+    return fail(net, BP_EINVAL, "bp_train_sequences: NULL or misaligned targets or mask");
+  return train_sequences(net, inputs_dev, targets_dev, cont_dev, mask_dev, n_steps, n_streams, steps_per_update, lr,
+                         momentum, sse_out);
+}
+
+int bp_forward_sequences(bp_net* net, const float* inputs_dev, const float* cont_dev, int64_t n_steps,
+                         int32_t n_streams, float* outputs_dev) {
+  if (check_net(net)) return BP_EINVAL;
+  int rc = check_seq(net, inputs_dev, cont_dev, n_steps, n_streams, "bp_forward_sequences");
+  if (rc) return rc;
+  if (n_steps > 0 && !outputs_dev) return fail(net, BP_EINVAL, "bp_forward_sequences: outputs_dev is NULL");
+  return forward_sequences(net, inputs_dev, cont_dev, n_steps, n_streams, outputs_dev);
 }
 
 int bp_set_sigmoid(bp_net* net, int32_t mode) {

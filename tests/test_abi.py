@@ -56,6 +56,9 @@ def test_null_net_is_rejected(bp):
     assert L.bp_train_batches_onehot(None, None, 7, None, 0, 1, 0.1, 0.9, None) == bp.BP_EINVAL
     assert L.bp_forward(None, None, 0, None) == bp.BP_EINVAL
     assert L.bp_forward_onehot(None, None, 7, 0, None) == bp.BP_EINVAL
+    assert L.bp_set_context(None, 0, None, None) == bp.BP_EINVAL
+    assert L.bp_train_sequences(None, None, None, None, None, 0, 1, 1, 0.1, 0.9, None) == bp.BP_EINVAL
+    assert L.bp_forward_sequences(None, None, None, 0, 1, None) == bp.BP_EINVAL
     assert L.bp_set_sigmoid(None, 1) == bp.BP_EINVAL
     assert L.bp_set_fault_limit(None, 1.0) == bp.BP_EINVAL
     assert L.bp_get_fault_count(None, None) == bp.BP_EINVAL

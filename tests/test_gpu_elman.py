@@ -1,0 +1,176 @@
+"""GPU parity of Elman-net training (section 10.5) against the CPU oracle.
+
+Same bars as the feed-forward path: weights after one pooled update (one
+window of steps) within 1e-5 relative max-abs per layer, per-epoch summed
+squared error within 1e-3, forward outputs within 1e-5.  Cases: the full
+1024-stream workload, a small one with a ragged stream count (200) and a
+short last window, context taken from two hidden layers, no context (=
+pooled feed-forward training over the patterns in step order), a fully
+masked stream (= no stream), and the argument checks.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1801_01554_amd import bp
+from paper_1801_01554_amd import workloads as wl
+from parity_util import SSE_TOL, W_TOL, rel, rel_maxabs
+
+pytestmark = pytest.mark.gpu
+FWD_TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU parity tests need a ROCm device"
+    bp.lib()
+    return torch.device("cuda:0")
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _d(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def _pair(w, ctx=True):
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    o = oracle.OracleNet(w.sizes, 64)
+    o.set_weights(w.weights.astype(np.float64))
+    if ctx:
+        net.set_context(w.ctx_layer, w.ctx_unit)
+        o.set_context(w.ctx_layer, w.ctx_unit)
+    return net, o
+
+
+def _dev_arrays(w, dev, steps=None):
+    T = w.spec.n_steps if steps is None else steps
+    return (_d(w.inputs[:T], dev), _d(w.targets[:T], dev), _d(w.cont[:T], dev), _d(w.mask[:T], dev))
+
+
+def _both(net, o, w, dev, steps=None, lr=None, mom=None):
+    s = w.spec
+    T = s.n_steps if steps is None else steps
+    lr = w.lr if lr is None else lr
+    mom = w.momentum if mom is None else mom
+    x, t, c, m = _dev_arrays(w, dev, T)
+    sg = net.train_sequences(x, t, c, m, s.steps_per_update, lr, mom)
+    so = o.train_sequences(w.inputs[:T], w.targets[:T], w.cont[:T], w.mask[:T], s.steps_per_update, lr, mom)
+    return sg, so
+
+
+@pytest.mark.parametrize("name", list(wl.SEQ_SPECS))
+def test_first_window_matches_oracle(dev, name):
+    w = wl.make_sequences(name)
+    s = w.spec
+    _say(f"case elman first window {name}: streams={s.n_streams} steps={s.steps_per_update}")
+    net, o = _pair(w)
+    sg, so = _both(net, o, w, dev, steps=s.steps_per_update)
+    ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
+    ev = rel_maxabs(w.sizes, net.get_momentum(), o.get_momentum())
+    _say(f"  weights rel err {ew}, momentum {ev}, sse {sg} vs {so}")
+    assert max(ew) <= W_TOL
+    assert rel(sg, so) <= SSE_TOL
+
+
+@pytest.mark.parametrize("name", list(wl.SEQ_SPECS))
+def test_epochs_match_oracle(dev, name):
+    w = wl.make_sequences(name)
+    s = w.spec
+    _say(f"case elman epochs {name}: {s.epochs} epoch(s) of {s.n_steps} steps x {s.n_streams} streams")
+    net, o = _pair(w)
+    for e in range(s.epochs):
+        sg, so = _both(net, o, w, dev)
+        _say(f"  epoch {e}: sse gpu {sg} oracle {so} rel {rel(sg, so):.3g}")
+        assert rel(sg, so) <= SSE_TOL
+    ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
+    _say(f"  final weights rel err {ew}")
+    assert max(ew) <= 10 * W_TOL
+
+
+@pytest.mark.parametrize("name", list(wl.SEQ_SPECS))
+def test_forward_sequences_match_oracle(dev, name):
+    w = wl.make_sequences(name)
+    _say(f"case elman forward {name}")
+    net, o = _pair(w)
+    x, _, c, _ = _dev_arrays(w, dev)
+    y = net.forward_sequences(x, c).cpu().numpy()
+    ref = o.forward_sequences(w.inputs, w.cont)
+    err = float(np.max(np.abs(y - ref)))
+    _say(f"  max abs err {err}")
+    assert err <= FWD_TOL
+
+
+def test_context_from_two_hidden_layers(dev):
+    spec = wl.SeqSpec("elman-two-layer", 10, (12, 9), 4, 6, 77, 23, 4, 3, 9, 0.01, 0.9, 2, 11)
+    w = wl.make_sequences(spec)
+    w.ctx_layer = np.array([1, 1, 1, 2, 2, 2], np.int32)
+    w.ctx_unit = np.array([0, 5, 11, 0, 4, 8], np.int32)
+    _say("case elman context from layers 1 and 2")
+    net, o = _pair(w)
+    for e in range(2):
+        sg, so = _both(net, o, w, dev)
+        _say(f"  epoch {e}: sse gpu {sg} oracle {so}")
+        assert rel(sg, so) <= SSE_TOL
+    assert max(rel_maxabs(w.sizes, net.get_weights(), o.get_weights())) <= 10 * W_TOL
+
+
+def test_no_context_equals_pooled_feedforward(dev):
+    w = wl.make_sequences("elman-20+48-48-12")
+    s = w.spec
+    sizes = (s.n_ext,) + s.hidden + (s.n_out,)
+    wt = np.random.default_rng(3).uniform(-0.3, 0.3, wl.num_weights(sizes)).astype(np.float32)
+    T, S = w.cont.shape
+    a, b = bp.Net(sizes), bp.Net(sizes)
+    a.set_weights(wt)
+    b.set_weights(wt)
+    ones = torch.ones((T, S), dtype=torch.float32, device=dev)
+    sa = a.train_sequences(_d(w.inputs, dev), _d(w.targets, dev), _d(w.cont, dev), ones, s.steps_per_update,
+                           0.01, 0.9)
+    sb = b.train_batches(_d(w.targets.reshape(T * S, -1), dev), s.steps_per_update * S, 0.01, 0.9,
+                         inputs=_d(w.inputs.reshape(T * S, -1), dev))
+    err = rel_maxabs(sizes, a.get_weights(), b.get_weights())
+    _say(f"  sequences vs batches: sse {sa} vs {sb}, weights rel diff {err}")
+    assert rel(sa, sb) <= 1e-6
+    assert max(err) <= 1e-6
+
+
+def test_masked_stream_is_no_stream(dev):
+    w = wl.make_sequences("elman-20+48-48-12")
+    s = w.spec
+    mask = w.mask.copy()
+    mask[:, 0] = 0.0
+    a, b = bp.Net(w.sizes), bp.Net(w.sizes)
+    for n in (a, b):
+        n.set_weights(w.weights)
+        n.set_context(w.ctx_layer, w.ctx_unit)
+    sa = a.train_sequences(_d(w.inputs, dev), _d(w.targets, dev), _d(w.cont, dev), _d(mask, dev),
+                           s.steps_per_update, w.lr, w.momentum)
+    sb = b.train_sequences(_d(w.inputs[:, 1:], dev), _d(w.targets[:, 1:], dev), _d(w.cont[:, 1:], dev),
+                           _d(mask[:, 1:], dev), s.steps_per_update, w.lr, w.momentum)
+    err = rel_maxabs(w.sizes, a.get_weights(), b.get_weights())
+    _say(f"  masked stream vs removed: sse {sa} vs {sb}, weights rel diff {err}")
+    assert rel(sa, sb) <= 1e-6 and max(err) <= 1e-6
+
+
+def test_sequence_arguments_are_checked(dev):
+    w = wl.make_sequences("elman-20+48-48-12")
+    net = bp.Net(w.sizes)
+    net.set_weights(w.weights)
+    for fl, fu in (([0], [0]), ([2], [0]), ([1], [48])):
+        with pytest.raises(bp.BPError):
+            net.set_context(fl, fu)
+    net.set_context(w.ctx_layer, w.ctx_unit)
+    x, t, c, m = _dev_arrays(w, dev)
+    with pytest.raises(bp.BPError):
+        net.train_sequences(x, t, c, m, 0, 0.1, 0.9)
+    before = net.get_weights()
+    assert net.train_sequences(x[:0], t[:0], c[:0], m[:0], 5, 0.1, 0.9) == 0.0
+    np.testing.assert_array_equal(net.get_weights(), before)
+    L = bp.lib()
+    assert L.bp_train_sequences(net._h, None, None, None, None, 3, 4, 1, 0.1, 0.9, None) == bp.BP_EINVAL
+    assert L.bp_train_sequences(net._h, None, None, None, None, 0, 0, 1, 0.1, 0.9, None) == bp.BP_EINVAL
