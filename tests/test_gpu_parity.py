@@ -165,6 +165,14 @@ def test_epoch_errors_dense_against_stored(dev, name):
         sg = _gpu_epoch(net, w, x, a, t, s.batch, w.lr, w.momentum)
         _say(f"  epoch {e}: sse gpu {sg:.9g} oracle {ref[e]:.9g} rel {rel(sg, ref[e]):.3g}")
         assert rel(sg, ref[e]) <= SSE_TOL
+    # final weights after the whole run, on the stored sample of indices: each
+    # of the run's pooled updates may add up to the one-update tolerance
+    st = g["storage64"]
+    idx = np.asarray(st["final_weight_sample_index"])
+    err = float(np.max(np.abs(net.get_weights()[idx] - np.asarray(st["final_weight_sample"])))) / st["final_weight_absmax"]
+    updates = s.epochs * ((w.n_patterns + s.batch - 1) // s.batch)
+    _say(f"  final weight sample after {updates} updates: max abs err / max |w| = {err:.3g}")
+    assert err <= updates * W_TOL
 
 
 # --------------------------------------------------------------------------- properties
