@@ -9,7 +9,10 @@ inputs resident in HBM).  The primary workload is the NETtalk-shaped
 patterns; its steps follow the epoch structure (40 updates per epoch, the
 last of 32 patterns).  The wide (1024-4096-1024, batch 4096) and deep
 (512-2048-2048-2048-64, batch 8192) dense nets run one full epoch each and
-are reported under "secondary".
+are reported under "secondary", with the Elman net (64 external inputs +
+256 context units, 256 hidden, 64 outputs; 1024 parallel sequence streams,
+an update every 8 steps) and the primary workload with the table sigmoid and
+with the range check of the summed changes switched on.
 
 value = connections x patterns presented / wall time (the paper's
 definition, section 7.1: bias connections included, update frequency and
@@ -39,6 +42,7 @@ PEAK_HBM = 8.0e12           # MI355X HBM3E, bytes/s
 PAPER_GF11_CPS = 9.01e8     # section 6.3, Table 1: 356 processors, tree summation
 PRIMARY = "nettalk-120-b512"
 SECONDARY = ("wide-1024-4096-1024", "deep-512-2048x3-64")
+SECONDARY_SEQ = ("elman-64+256-256-64",)
 GEMM_KINDS = ("forward", "output", "backward", "change")
 KERNEL_NAMES = {
     "forward": "gemm_kernel<..., EpiSigmoid>",
@@ -53,12 +57,14 @@ KERNEL_NAMES = {
     "fused_fb": "small_fwdbwd_kernel",
     "fused_update": "small_update_kernel",
     "output_finish": "output_finish_kernel",
+    "seq_in": "seq_assemble_kernel",
 }
 SMALL_MAX_HIDDEN, SMALL_MAX_OUT, SMALL_MAX_ACTIVE = 256, 64, 32   # the library's fused-path limits
 
 
-def kind_work(sizes, rows, onehot, n_active, splits_of):
-    """Algorithmic (flops, HBM bytes) of each kernel kind for one update over `rows` patterns."""
+def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
+    """Algorithmic (flops, HBM bytes) of each kernel kind for one update over `rows` patterns
+    (parts: "fwd" the forward pass and output deltas, "bwd" the hidden deltas, changes and updates)."""
     w = {}
 
     def add(kind, f, b):
@@ -74,28 +80,45 @@ def kind_work(sizes, rows, onehot, n_active, splits_of):
         add("fused_update", R * (2 * (H + 1) * O + H * (n_active + 1)),
             4 * (R * n_active + 2 * R * H + R * O) + 16 * ((n0 + 1) * H + (H + 1) * O))
         return w
+    fwd, bwd = "fwd" in parts, "bwd" in parts
     for l in range(L):
         ni, no = sizes[l], sizes[l + 1]
         if l == 0 and onehot:
             add("gather", R * no * (n_active + 1), 4 * (R * n_active + (ni + 1) * no + R * no))
             add("scatter", R * no * (n_active + 1), 4 * (R * n_active + R * no) + 16 * (ni + 1) * no)
         else:
-            if l == L - 1 and splits_of(rows, no, ni) > 1:
+            if fwd and l == L - 1 and splits_of(rows, no, ni) > 1:
                 add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no))
                 add("output_finish", 6 * R * no, 4 * (2 * R * no + no))
-            elif l == L - 1:
+            elif fwd and l == L - 1:
                 add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + 2 * R * no))
-            else:
+            elif fwd:
                 add("forward", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + R * no))
             upd = 16.0 * ni * no
-            if splits_of(ni, no, rows) > 1:
+            if bwd and splits_of(ni, no, rows) > 1:
                 add("change", 2 * R * ni * no, 4 * (R * ni + R * no))
                 add("splitk", 0.0, upd)
-            else:
+            elif bwd:
                 add("change", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
-            add("bias", R * no, 4 * -(-rows // 128) * no + 16 * no)
-        if l >= 1:
+            if bwd:
+                add("bias", R * no, 4 * -(-rows // 128) * no + 16 * no)
+        if l >= 1 and bwd:
             add("backward", 2 * R * no * ni, 4 * (R * no + ni * no + 2 * R * ni))
+    return w
+
+
+def seq_kind_work(sizes, n_ctx, S, steps, splits_of):
+    """Algorithmic (flops, HBM bytes) per kind of one Elman window: `steps` forward steps of S
+    patterns (with the input assembly), then one backward pass and update over steps x S rows."""
+    n_ext = sizes[0] - n_ctx
+    w = {"seq_in": (0.0, 4.0 * steps * S * (n_ext + 1 + n_ctx + -(-sizes[0] // 4) * 4))}
+    for _ in range(steps):
+        for k, (f, b) in kind_work(sizes, S, False, 0, splits_of, ("fwd",)).items():
+            f0, b0 = w.get(k, (0.0, 0.0))
+            w[k] = (f0 + f, b0 + b)
+    for k, (f, b) in kind_work(sizes, steps * S, False, 0, splits_of, ("bwd",)).items():
+        f0, b0 = w.get(k, (0.0, 0.0))
+        w[k] = (f0 + f, b0 + b)
     return w
 
 
@@ -127,7 +150,8 @@ def step_rows(spec, calls):
     return rows
 
 
-def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
+def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None):
+    """Times `steps` pooled updates of a named workload (variant: "table sigmoid" or "range check")."""
     spec = wl.SPECS[name]
     t0 = time.time()
     w = wl.make(name)
@@ -137,6 +161,12 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
     x = torch.from_numpy(w.inputs).to(dev) if w.inputs is not None else None
     a = torch.from_numpy(w.active).to(dev) if w.active is not None else None
     net = bp.Net(w.sizes)
+    if variant == "table sigmoid":
+        net.set_sigmoid(bp.BP_SIGMOID_TABLE)
+    elif variant == "range check":
+        net.set_fault_limit(1e6)
+    elif variant is not None:
+        raise ValueError(variant)
 
     def run(calls):
         for p0, n, _ in calls:
@@ -160,7 +190,8 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     secs = ev0.elapsed_time(ev1) / 1e3
-    log(f"[{name}] {steps} steps, {patterns} patterns in {secs * 1e3:.2f} ms (wall {wall * 1e3:.2f} ms)")
+    log(f"[{name}{' + ' + variant if variant else ''}] {steps} steps, {patterns} patterns in {secs * 1e3:.2f} ms "
+        f"(wall {wall * 1e3:.2f} ms)")
 
     # profile pass: the same steps with every launch bracketed by events
     net.set_weights(w.weights)
@@ -178,6 +209,22 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
         for k, (f, b) in kind_work(w.sizes, r, w.active is not None, 7, choose_splits).items():
             f0, b0 = work.get(k, (0.0, 0.0))
             work[k] = (f0 + f, b0 + b)
+    kernels, roof, gemm_f, gemm_ms = summarize_kernels(rep, work, name)
+    res = {
+        "workload": name, "net": "-".join(map(str, w.sizes)), "batch": spec.batch, "patterns": patterns,
+        "steps": steps, "warmup": warmup, "seconds": secs, "ms_per_step": secs * 1e3 / steps, "value": cps,
+        "mfma_peak_frac": flops_step / secs / PEAK_FP32_MFMA,
+        "gemm_mfma_frac": (gemm_f / (gemm_ms / 1e3) / PEAK_FP32_MFMA) if gemm_ms > 0 else None,
+        "us_per_update": secs * 1e6 / steps, "roofline": roof, "kernels": kernels,
+        "kernel_time_ms": sum(v["total_ms"] for v in kernels.values()),
+    }
+    if variant:
+        res["variant"] = variant
+    return res, w
+
+
+def summarize_kernels(rep, work, name):
+    """Per-kind kernel table and the roofline entry of the dominant kind."""
     kernels = {}
     for k, (cnt, ms) in rep.items():
         if cnt == 0:
@@ -201,13 +248,61 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log):
             "traffic": traffic_for(name, dom)}
     gemm_ms = sum(kernels[k]["total_ms"] for k in GEMM_KINDS if k in kernels)
     gemm_f = sum(work.get(k, (0, 0))[0] for k in GEMM_KINDS)
+    return kernels, roof, gemm_f, gemm_ms
+
+
+def run_seq_workload(name, epochs, torch, bp, wl, metrics, log):
+    """Elman training: `epochs` whole passes over the sequence streams, after one untimed epoch."""
+    spec = wl.SEQ_SPECS[name]
+    t0 = time.time()
+    w = wl.make_sequences(name)
+    log(f"[{name}] generated {spec.n_steps} steps x {spec.n_streams} streams in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    x, t, c, m = (torch.from_numpy(a).to(dev) for a in (w.inputs, w.targets, w.cont, w.mask))
+    net = bp.Net(w.sizes)
+    net.set_context(w.ctx_layer, w.ctx_unit)
+
+    def run():
+        for _ in range(epochs):
+            net.train_sequences(x, t, c, m, spec.steps_per_update, w.lr, w.momentum, want_sse=False)
+
+    net.set_weights(w.weights)
+    net.train_sequences(x, t, c, m, spec.steps_per_update, w.lr, w.momentum, want_sse=False)   # warmup epoch
+    net.set_weights(w.weights)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    run()
+    ev1.record()
+    torch.cuda.synchronize()
+    secs = ev0.elapsed_time(ev1) / 1e3
+    windows = -(-spec.n_steps // spec.steps_per_update) * epochs
+    real = int(w.mask.sum()) * epochs
+    log(f"[{name}] {epochs} epoch(s), {windows} updates, {real} patterns ({spec.n_steps * spec.n_streams * epochs} "
+        f"with padding) in {secs * 1e3:.2f} ms")
+    net.set_weights(w.weights)
+    net.profile(True)
+    run()
+    rep = net.profile_report()
+    net.profile(False)
+    net.close()
+    work = {}
+    for w0 in range(0, spec.n_steps, spec.steps_per_update):
+        steps = min(spec.steps_per_update, spec.n_steps - w0)
+        for k, (f, b) in seq_kind_work(w.sizes, spec.n_ctx, spec.n_streams, steps, choose_splits).items():
+            f0, b0 = work.get(k, (0.0, 0.0))
+            work[k] = (f0 + epochs * f, b0 + epochs * b)
+    kernels, roof, gemm_f, gemm_ms = summarize_kernels(rep, work, name)
+    W = metrics.num_weights(w.sizes)
+    flops = sum(f for f, _ in work.values())
     res = {
-        "workload": name, "net": "-".join(map(str, w.sizes)), "batch": spec.batch, "patterns": patterns,
-        "steps": steps, "warmup": warmup, "seconds": secs, "ms_per_step": secs * 1e3 / steps, "value": cps,
-        "mfma_peak_frac": flops_step / secs / PEAK_FP32_MFMA,
+        "workload": name, "net": "-".join(map(str, w.sizes)), "streams": spec.n_streams,
+        "steps_per_epoch": spec.n_steps, "steps_per_update": spec.steps_per_update, "epochs": epochs,
+        "patterns": real, "patterns_with_padding": spec.n_steps * spec.n_streams * epochs, "seconds": secs,
+        "value": W * real / secs, "unit": "connections/s (sequence patterns, padding excluded)",
+        "us_per_update": secs * 1e6 / windows, "mfma_peak_frac": flops / secs / PEAK_FP32_MFMA,
         "gemm_mfma_frac": (gemm_f / (gemm_ms / 1e3) / PEAK_FP32_MFMA) if gemm_ms > 0 else None,
-        "us_per_update": secs * 1e6 / steps, "roofline": roof, "kernels": kernels,
-        "kernel_time_ms": sum(v["total_ms"] for v in kernels.values()),
+        "roofline": roof, "kernels": kernels, "kernel_time_ms": sum(v["total_ms"] for v in kernels.values()),
     }
     return res, w
 
@@ -218,7 +313,7 @@ COPY_BYTES = 1 << 30        # one copy of 1 GiB for the counter calibration
 
 def kernel_source_sha():
     h = hashlib.sha256()
-    for f in ("bp_kernels.hip", "bp_small.hip"):
+    for f in ("bp_device.h", "bp_kernels.hip", "bp_small.hip", "bp_seq.hip"):
         h.update(open(os.path.join(ROOT, "paper_1801_01554_amd", "csrc", f), "rb").read())
     return h.hexdigest()
 
@@ -428,6 +523,14 @@ def main():
             secondary.append(r)
             del w2
             torch.cuda.empty_cache()
+        for name in SECONDARY_SEQ:
+            r, w2 = run_seq_workload(name, 1, torch, bp, wl, metrics, log)
+            secondary.append(r)
+            del w2
+            torch.cuda.empty_cache()
+        for variant in ("table sigmoid", "range check"):
+            r, _ = run_workload(args.workload, steps, warmup, torch, bp, wl, metrics, log, variant=variant)
+            secondary.append(r)
 
     line = {
         "metric": METRIC, "value": prim["value"], "unit": "connections/s", "n_gpus": 1, "steps": steps,

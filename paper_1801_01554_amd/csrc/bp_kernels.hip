@@ -35,6 +35,15 @@ constexpr int kThreads = 256;
 // deltas they produce (colsum[tile row][n]; the bias-row change of the layer
 // below is the sum of these over the tile rows).  `tab` is the sigmoid table
 // (nullptr: exact logistic).
+//
+// load() returns the per-element operands an epilogue reads from memory
+// (Pre).  The kernel loads them for a whole 32 x 32 block before the
+// block's first store, so the loads are in flight together instead of each
+// waiting behind the stores of the elements before it (which the compiler
+// must assume may alias them).
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+struct NoPre {};
 
 struct EpiSigmoid {
   const float* bias;
@@ -44,8 +53,10 @@ struct EpiSigmoid {
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
   static constexpr bool kFaults = false;
+  using Pre = NoPre;
+  __device__ Pre load(int, int) const { return {}; }
   __device__ float column(int n) const { return bias[n]; }
-  __device__ float apply(int m, int n, float acc, float b, float&) const {
+  __device__ float apply(int m, int n, float acc, float b, Pre, float&) const {
     out[(size_t)m * ldo + n] = unit_sigma(acc + b, tab);
     return 0.f;
   }
@@ -65,11 +76,13 @@ struct EpiOutputDelta {
   static constexpr bool kSSE = true;
   static constexpr bool kColSum = true;
   static constexpr bool kFaults = false;
+  using Pre = f32x2;     // target, mask
+  __device__ Pre load(int m, int n) const { return {T[(size_t)m * ldt + n], mask ? mask[m] : 1.0f}; }
   __device__ float column(int n) const { return bias[n]; }
-  __device__ float apply(int m, int n, float acc, float b, float& sse) const {
+  __device__ float apply(int m, int n, float acc, float b, Pre tm, float& sse) const {
     const float y = unit_sigma(acc + b, tab);
-    float e = T[(size_t)m * ldt + n] - y;
-    if (mask) e *= mask[m];
+    float e = tm.x - y;
+    if (mask) e *= tm.y;
     sse += e * e;
     const float d = e * y * (1.0f - y);
     delta[(size_t)m * ldd + n] = d;
@@ -87,9 +100,10 @@ struct EpiHiddenDelta {
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = true;
   static constexpr bool kFaults = false;
+  using Pre = float;     // activation
+  __device__ Pre load(int m, int n) const { return act[(size_t)m * lda + n]; }
   __device__ float column(int) const { return 0.f; }
-  __device__ float apply(int m, int n, float acc, float, float&) const {
-    const float a = act[(size_t)m * lda + n];
+  __device__ float apply(int m, int n, float acc, float, Pre a, float&) const {
     const float d = acc * (a * (1.0f - a));
     out[(size_t)m * ldo + n] = d;
     return d;
@@ -106,15 +120,20 @@ struct EpiUpdate {
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
   static constexpr bool kFaults = true;
+  using Pre = f32x2;     // momentum, weight
+  __device__ Pre load(int m, int n) const {
+    const size_t i = (size_t)m * ldw + n;
+    return {V[i], W[i]};
+  }
   __device__ float column(int) const { return 0.f; }
-  __device__ float apply(int m, int n, float acc, float, float& nf) const {
+  __device__ float apply(int m, int n, float acc, float, Pre vw, float& nf) const {
     const size_t i = (size_t)m * ldw + n;
     int f = 0;
     const float g = checked_change(acc, limit, f);
     nf += (float)f;
-    const float v = lr * g + mom * V[i];
+    const float v = lr * g + mom * vw.x;
     V[i] = v;
-    W[i] = W[i] + v;
+    W[i] = vw.y + v;
     return 0.f;
   }
 };
@@ -127,8 +146,10 @@ struct EpiPartial {
   static constexpr bool kSSE = false;
   static constexpr bool kColSum = false;
   static constexpr bool kFaults = false;
+  using Pre = NoPre;
+  __device__ Pre load(int, int) const { return {}; }
   __device__ float column(int) const { return 0.f; }
-  __device__ float apply(int m, int n, float acc, float, float&) const {
+  __device__ float apply(int m, int n, float acc, float, Pre, float&) const {
     P[blockIdx.z * split_stride + (size_t)m * ldp + n] = acc;
     return 0.f;
   }
@@ -343,6 +364,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
   float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
+  // The per-element operands of each 32 x 32 block are loaded together
+  // (clamped, always valid addresses; values outside the matrix are never
+  // used) before the block's stores: one memory round trip per block, with
+  // few extra registers.
   float csum[T::TN];
 #pragma unroll
   for (int j = 0; j < T::TN; ++j) {
@@ -352,10 +377,14 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       const float cv = epi.column(n);
 #pragma unroll
       for (int i = 0; i < T::TM; ++i) {
+        typename Epi::Pre pre[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          pre[e] = epi.load(min(m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), M - 1), n);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-          if (m < M) csum[j] += epi.apply(m, n, acc[i][j][e], cv, sse);
+          if (m < M) csum[j] += epi.apply(m, n, acc[i][j][e], cv, pre[e], sse);
         }
       }
     }
@@ -479,17 +508,21 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
   const int m0 = blockIdx.x * 128 + wave * R;
   float sse = 0.f, csum = 0.f;
   if (n < N) {
+    // rows are clamped to M - 1 so that every load is unconditional (all in
+    // flight together); rows past M are never used
     const float b = bias[n];
-    float z[R], t[R];
+    float z[R], t[R], mk[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
+      const int m = min(m0 + r, M - 1);
       z[r] = 0.f;
-      t[r] = m0 + r < M ? T[(size_t)(m0 + r) * ldt + n] : 0.f;
+      t[r] = T[(size_t)m * ldt + n];
+      mk[r] = mask ? mask[m] : 1.0f;
     }
     for (int sp = 0; sp < splits; ++sp) {
       float v[R];
 #pragma unroll
-      for (int r = 0; r < R; ++r) v[r] = m0 + r < M ? P[sp * stride + (size_t)(m0 + r) * ldp + n] : 0.f;
+      for (int r = 0; r < R; ++r) v[r] = P[sp * stride + (size_t)min(m0 + r, M - 1) * ldp + n];
 #pragma unroll
       for (int r = 0; r < R; ++r) z[r] += v[r];
     }
@@ -498,7 +531,7 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
       if (m0 + r >= M) break;
       const float y = unit_sigma(z[r] + b, tab);
       float e = t[r] - y;
-      if (mask) e *= mask[m0 + r];
+      if (mask) e *= mk[r];
       sse += e * e;
       const float d = e * y * (1.0f - y);
       delta[(size_t)(m0 + r) * ldd + n] = d;
