@@ -358,7 +358,7 @@ def summarize_stats(src, out, title, note, cmd):
              "|---|---|---|---|---|---|---|"]
     for r in csv.DictReader(open(src)):
         name = r["Name"].replace("bpk::(anonymous namespace)::", "")
-        m = re.search(r"(gemm_kernel<[^>]*>|\w+_kernel|fillBufferAligned)", name)
+        m = re.search(r"(\w+_kernel(?:<[^>]*>)?|fillBufferAligned|copyBuffer)", name)
         short = m.group(1) if m else name[:60]
         lines.append(f"| `{short}` | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | "
                      f"{float(r['Percentage']):.1f} | {r['MinNs']} | {r['MaxNs']} |")
@@ -504,6 +504,17 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a ROCm device"
     bp.lib()
+    if args.workload in wl.SEQ_SPECS:
+        # an Elman workload on its own (profiling runs): one epoch per step
+        epochs = args.steps if args.steps is not None else 1
+        r, _ = run_seq_workload(args.workload, epochs, torch, bp, wl, metrics, log)
+        print(json.dumps({"metric": METRIC, "value": r["value"], "unit": "connections/s", "n_gpus": 1,
+                          "steps": epochs, "warmup": 1, "ms_per_step": r["seconds"] * 1e3 / epochs,
+                          "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+                          "data": "synthetic", "config": {"workload": args.workload, "net": r["net"],
+                                                          "parallelism": "single GPU"},
+                          "roofline": r["roofline"], "kernels": r["kernels"]}), flush=True)
+        return
     spec = wl.SPECS[args.workload]
     per_epoch = -(-spec.n_patterns // spec.batch)
     steps = args.steps if args.steps is not None else per_epoch * spec.epochs
