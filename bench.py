@@ -101,7 +101,7 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
             elif bwd:
                 add("change", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
             if bwd:
-                add("bias", R * no, 4 * -(-rows // 128) * no + 16 * no)
+                add("bias", R * no, 4 * -(-rows // 64) * no + 16 * no)
         if l >= 1 and bwd:
             add("backward", 2 * R * no * ni, 4 * (R * no + ni * no + 2 * R * ni))
     return w
@@ -123,8 +123,9 @@ def seq_kind_work(sizes, n_ctx, S, steps, splits_of):
 
 
 def choose_splits(M, N, K):
-    """Mirror of the library's split-K choice (128 x 128 tiles), for work accounting only."""
-    tiles = -(-M // 128) * -(-N // 128)
+    """Mirror of the library's split-K choice, for work accounting only."""
+    t128 = -(-M // 128) * -(-N // 128)
+    tiles = t128 if (t128 >= 256 or K >= 1024) else -(-M // 64) * -(-N // 64)
     if K < 1024 or tiles >= 512:
         return 1
     s = -(-512 // tiles)

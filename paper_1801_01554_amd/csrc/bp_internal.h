@@ -54,7 +54,7 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
 // (mask == nullptr: no mask);
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of
 // block b (b < output_delta_blocks(M, N, K)); colsum[t][n] = sum of delta
-// over rows [128 t, 128 t + 128) (t < colsum_rows(M)).  With
+// over rows [64 t, 64 t + 64) (t < colsum_rows(M)).  With
 // output_delta_splits(M, N, K) > 1 the product writes split partials to `ws`
 // (output_delta_workspace floats) and output_finish applies the epilogue.
 int output_delta_blocks(int M, int N, int K);

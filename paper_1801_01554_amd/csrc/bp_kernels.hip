@@ -390,10 +390,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
     }
   }
   if constexpr (Epi::kColSum) {
-    // Column sums per 128-row group of the tile.  Lanes h = 0, 1 hold the
-    // same column (different rows); the wave rows of a group are then added
-    // in a fixed order.
-    constexpr int kGroups = BM / 128, kWaveRowsPerGroup = 256 / BM;
+    // Column sums per 64-row group of the tile (a 128-row tile has two, one
+    // per wave row; a 64-row tile one, over both wave rows).  Lanes h = 0, 1
+    // hold the same column (different rows); the wave rows of a group are
+    // then added in a fixed order.
+    static_assert(BM == 64 || BM == 128, "column-sum groups assume 64- or 128-row tiles");
+    constexpr int kGroups = BM / 64, kWaveRowsPerGroup = 2 / kGroups;
     __shared__ float cs[2][BN];
 #pragma unroll
     for (int j = 0; j < T::TN; ++j) {
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
       const int crow = tm * kGroups + g;
-      if (crow * 128 >= M) break;
+      if (crow * 64 >= M) break;
       for (int c = threadIdx.x; c < BN; c += kThreads) {
         if (n0 + c >= N) continue;
         float v = cs[g * kWaveRowsPerGroup][c];
@@ -430,13 +432,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   }
 }
 
-// Tile configuration: 128 x 128 x 32, wave tile 64 x 64, two blocks per CU
-// (72 KB of LDS with both buffers).  (A 256 x 128 x 16 tile, one block per
-// CU round for more products, measured slower on the wide and deep nets.)
-constexpr int kTileM = 128, kTileN = 128, kTileK = 32;
+// Tile configurations: 128 x 128 x 32 (wave tile 64 x 64, two blocks per
+// CU, 72 KB of LDS with both buffers) for products with at least one tile
+// per CU or deep enough in K for split-K to fill the chip; 64 x 64 x 32
+// (wave tile 32 x 32) for the other, small products, which gives them four
+// times the blocks (and wastes less of an edge tile).  (A 256 x
+// 128 x 16 tile, one block per CU round for more products, measured slower
+// on the wide and deep nets.)
+constexpr int kTileK = 32;
 constexpr int kChunkAlign = kTileK;   // split-K chunks are multiples of BK
+constexpr int kCUs = 256;
 
-inline int tile_count(int M, int N) { return ((M + kTileM - 1) / kTileM) * ((N + kTileN - 1) / kTileN); }
+inline int tiles_of(int M, int N, int t) { return ((M + t - 1) / t) * ((N + t - 1) / t); }
+// Edge of the square tile an M x N product summed over K uses.
+inline int tile_edge(int M, int N, int K) { return (tiles_of(M, N, 128) >= kCUs || K >= 1024) ? 128 : 64; }
+inline int tile_count(int M, int N, int K) { return tiles_of(M, N, tile_edge(M, N, K)); }
 
 template <int BM, int BN, int BK, bool A_KM, bool B_NK, class Epi>
 hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
@@ -462,7 +472,9 @@ hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, i
 template <bool A_KM, bool B_NK, class Epi>
 hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K, int splits,
                       int k_chunk, const Epi& epi) {
-  return launch_gemm<kTileM, kTileN, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
+  if (tile_edge(M, N, K) == 128)
+    return launch_gemm<128, 128, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
+  return launch_gemm<64, 64, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
 }
 
 // --------------------------------------------------------------------------
@@ -491,8 +503,9 @@ __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __
 // the output-delta epilogue (bias, sigma, e = T - y, delta = e y (1 - y)).
 // Block (x, y) covers rows [128 x, 128 x + 128) and columns [64 y, 64 y + 64)
 // with 16 waves; lane = column, wave w = rows 8 w .. 8 w + 7 (their loads
-// issued together).  Writes the block's error partial and the 128-row column
-// sums of the deltas (the tiling of the fused epilogue), both in wave order.
+// issued together).  Writes the block's error partial and the 64-row column
+// sums of the deltas (waves 0-7 and 8-15; the grouping of the fused
+// epilogue), both in wave order.
 constexpr int kFin = 1024;
 __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __restrict__ P, int splits, size_t stride,
                                                              int ldp, int M, int N, const float* __restrict__ bias,
@@ -542,10 +555,11 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
   for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
   if (lane == 0) red[wave] = sse;
   __syncthreads();
-  if (wave == 0 && n < N) {
-    float c = cs[0][lane];
-    for (int w = 1; w < W; ++w) c += cs[w][lane];
-    colsum[(size_t)blockIdx.x * ldcs + n] = c;
+  if (wave < 2 && n < N && blockIdx.x * 128 + wave * 64 < M) {
+    constexpr int kHalf = W / 2;
+    float c = cs[wave * kHalf][lane];
+    for (int w = 1; w < kHalf; ++w) c += cs[wave * kHalf + w][lane];
+    colsum[(size_t)(2 * blockIdx.x + wave) * ldcs + n] = c;
   }
   if (threadIdx.x == 0) {
     double tt = 0.0;
@@ -711,7 +725,7 @@ __global__ __launch_bounds__(kRed) void sse_reduce_kernel(const double* __restri
 // K-splits for a product with few output tiles: enough blocks for two per
 // CU (512), each split at least 256 deep in K.
 int choose_splits(int M, int N, int K) {
-  const int tiles = tile_count(M, N);
+  const int tiles = tile_count(M, N, K);
   if (K < 1024 || tiles >= 512) return 1;
   int s = (512 + tiles - 1) / tiles;
   const int max_s = K / 256;
@@ -736,11 +750,11 @@ LaunchEvents& launch_events() {
   return ev;
 }
 
-int colsum_rows(int M) { return (M + 127) / 128; }
+int colsum_rows(int M) { return (M + 63) / 64; }
 
 int output_delta_blocks(int M, int N, int K) {
   if (choose_output_splits(M, N, K) > 1) return ((M + 127) / 128) * ((N + 63) / 64);
-  return tile_count(M, N);
+  return tile_count(M, N, K);
 }
 
 size_t output_delta_workspace(int M, int N, int K) {

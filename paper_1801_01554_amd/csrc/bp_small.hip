@@ -27,7 +27,7 @@
 namespace bpk {
 namespace {
 
-constexpr int kT = 256;        // threads per forward/backward block
+constexpr int kT = 1024;       // threads per forward/backward block (16 waves)
 constexpr int kTU = 1024;      // threads per update block (16 waves)
 constexpr int kWU = kTU / 64;
 constexpr int kMaxP = 8;       // patterns per forward/backward block
@@ -48,8 +48,18 @@ __device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int&
 // hidden activations [P][H], the output deltas [P][O], the targets [P][O]
 // and the active indices [P][n_active] of the block's patterns.
 //
-// The kernel has two rounds of global loads: (1) indices, targets and W1,
-// all independent; (2) the gathered W0 rows of all the block's patterns.
+// 1024 threads (16 waves, four per SIMD) per block of P patterns: every
+// phase is spread over all of them, so each lane's chain of dependent LDS
+// reads is short and the waves of a SIMD hide each other's latencies.
+//   round 1   indices, targets and W1: independent loads, all in flight;
+//   gather    one (pattern, hidden unit) pair per thread: bias + the active
+//             rows of W0, in index order -> sigma;
+//   output    each output (p, c) summed by 2^lg adjacent lanes, lane k over
+//             the hidden units k, k + 2^lg, ..., combined by a butterfly;
+//   deltas    each hidden delta (p, j) summed by 2^lq adjacent lanes, lane k
+//             over the outputs k, k + 2^lq, ..., combined by a butterfly.
+// The strided shares walk LDS by pointer increments, with no clamped or
+// guarded reads in the inner loops.
 // P (patterns per block) and TAB (table sigmoid) are template parameters so
 // that each instantiation holds only the code it runs: these kernels are
 // short enough that instruction-cache misses at launch are a visible part of
@@ -75,67 +85,60 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   const int np = min(P, rows - p0);
   const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
-  // round 1 (np * n_active <= kT and np * O <= 2 kT by the path's limits)
+  // round 1 (np * n_active <= 256 and np * O <= 512 <= kT by the path's
+  // limits).  Every load reads a clamped, valid address and the predicate
+  // only selects the value: no load sits behind a branch, so all are in
+  // flight together.  (Rows of act and of T are contiguous.)
   {
     const int ni = np * n_active, nt = np * O;
-    // Every load below reads a clamped, valid address and the predicate only
-    // selects the value: no load sits behind a branch, so all are in flight
-    // together.  (Rows of act and of T are contiguous.)
     const int iv = act[(size_t)p0 * n_active + min(tid, ni - 1)];
     const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
-    const float t1 = T[(size_t)p0 * O + min(tid + kT, nt - 1)];
     // W1: lane column c = tid % cw, rows tid / cw + k (kT / cw)
     const int cw = O <= 32 ? 32 : 64, rpp = kT / cw;
     const int c = tid & (cw - 1), jt = tid / cw;
-    for (int k0 = 0; k0 * rpp <= H; k0 += 16) {
-      float v[16];
+    for (int k0 = 0; k0 * rpp <= H; k0 += 4) {
+      float v[4];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+      for (int u = 0; u < 4; ++u) {
         const int j = jt + (k0 + u) * rpp;
         v[u] = W1[(size_t)min(j, H) * ldw1 + min(c, O - 1)];
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+      for (int u = 0; u < 4; ++u) {
         const int j = jt + (k0 + u) * rpp;
         if (c < O && j <= H) w1s[j * S1 + c] = v[u];
       }
     }
     if (tid < ni) idx[tid] = iv;
     if (tid < nt) ts[tid] = t0;
-    if (tid + kT < nt) ts[tid + kT] = t1;
   }
   __syncthreads();
-  // round 2: hidden layer, net = bias + sum of the active rows of W0 (in index order)
-  for (int j = tid; j < H; j += kT) {
-    const float b = W0[(size_t)n0 * ldw0 + j];
-    float v[P][8];
+  // gather: net = bias + the active rows of W0 (in index order)
+  for (int t = tid; t < np * H; t += kT) {
+    int p = 0, j = 0;
+    divmod(t, H, inv_H, p, j);
+    const int* ip = idx + p * n_active;
+    float v[8];
 #pragma unroll
-    for (int p = 0; p < P; ++p)
+    for (int u = 0; u < 8; ++u) v[u] = W0[(size_t)ip[min(u, n_active - 1)] * ldw0 + j];
+    float net = W0[(size_t)n0 * ldw0 + j];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        v[p][u] = W0[(size_t)idx[min(p, np - 1) * n_active + min(u, n_active - 1)] * ldw0 + j];
-#pragma unroll
-    for (int p = 0; p < P; ++p) {
-      if (p >= np) break;
-      float net = b;
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (u < n_active) net += v[p][u];
-      for (int k = 8; k < n_active; ++k) net += W0[(size_t)idx[p * n_active + k] * ldw0 + j];
-      const float h = TAB ? logistic_table(net, tab) : logistic(net);
-      hs[p * H + j] = h;
-      A1[(size_t)(p0 + p) * lda1 + j] = h;
-    }
+    for (int u = 0; u < 8; ++u)
+      if (u < n_active) net += v[u];
+    for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + j];
+    const float h = TAB ? logistic_table(net, tab) : logistic(net);
+    hs[t] = h;
+    A1[(size_t)(p0 + p) * lda1 + j] = h;
   }
   __syncthreads();
   // Output layer, output deltas and squared error.  Each output (p, c) is
-  // computed by `lpo` adjacent lanes, lane k summing a contiguous share of
-  // the hidden units; the shares are combined by a butterfly, which gives
-  // every lane of the group the same (commutative) sum.
+  // computed by `lpo` adjacent lanes; the lanes' partial sums are combined by
+  // a butterfly, which gives every lane of the group the same (commutative)
+  // sum.
   float sse = 0.f;
   {
     const int nout = np * O;
-    int lg = 3;
+    int lg = 4;
     while (lg > 0 && (nout << lg) > kT) --lg;
     const int lpo = 1 << lg;
     for (int t0 = 0; t0 < (nout << lg); t0 += kT) {
@@ -145,19 +148,28 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       divmod(q, O, inv_O, p, c);
       float z = 0.f;
       if (q < nout) {
-        const float* h = hs + p * H;
-        const int j0 = (H * part) >> lg, j1 = (H * (part + 1)) >> lg;
-        for (int j = j0; j < j1; j += 8) {
-          float hv[8], wv[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int jc = min(j + u, j1 - 1);
-            hv[u] = j + u < j1 ? h[jc] : 0.f;
-            wv[u] = w1s[jc * S1 + c];
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) z += hv[u] * wv[u];
+        const float* hp = hs + p * H + part;           // units part, part + lpo, ...
+        const float* wp = w1s + part * S1 + c;
+        const int n = (H - part + lpo - 1) >> lg;       // units of this lane
+        const int ws = lpo * S1;
+        float z1 = 0.f;
+        int k = 0;
+        for (; k + 4 <= n; k += 4) {
+          const float h0 = hp[0], h1 = hp[lpo], h2 = hp[2 * lpo], h3 = hp[3 * lpo];
+          const float w0 = wp[0], w1 = wp[ws], w2 = wp[2 * ws], w3 = wp[3 * ws];
+          z += h0 * w0;
+          z1 += h1 * w1;
+          z += h2 * w2;
+          z1 += h3 * w3;
+          hp += 4 * lpo;
+          wp += 4 * ws;
         }
+        for (; k < n; ++k) {
+          z += hp[0] * wp[0];
+          hp += lpo;
+          wp += ws;
+        }
+        z += z1;
       }
       for (int m = 1; m < lpo; m <<= 1) z += __shfl_xor(z, m, 64);
       if (q < nout && part == 0) {
@@ -172,26 +184,48 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
     }
   }
   __syncthreads();
-  // hidden deltas (W1 before its update, bias row excluded): one thread per (p, j)
-  for (int t = tid; t < np * H; t += kT) {
-    int p, j;
-    divmod(t, H, inv_H, p, j);
-    const float* wr = w1s + j * S1;
-    const float* d = d2s + p * O;
-    float s = 0.f;
-    for (int c = 0; c < O; c += 8) {
-      float wv[8], dv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int cc = min(c + u, O - 1);
-        wv[u] = wr[cc];
-        dv[u] = c + u < O ? d[cc] : 0.f;
+  // hidden deltas (W1 before its update, bias row excluded): each (p, j) by
+  // `lpd` adjacent lanes, each summing a contiguous share of the outputs
+  {
+    const int nh = np * H;
+    int lq = 3;
+    while (lq > 0 && (nh << lq) > kT) --lq;
+    const int lpd = 1 << lq;
+    for (int t0 = 0; t0 < (nh << lq); t0 += kT) {
+      const int t = t0 + tid;
+      const int q = t >> lq, part = t & (lpd - 1);
+      int p = 0, j = 0;
+      divmod(q, H, inv_H, p, j);
+      float sd = 0.f;
+      if (q < nh) {
+        const float* wp = w1s + j * S1 + part;         // outputs part, part + lpd, ...
+        const float* dp = d2s + p * O + part;
+        const int n = (O - part + lpd - 1) >> lq;
+        float s1 = 0.f;
+        int k = 0;
+        for (; k + 4 <= n; k += 4) {
+          const float w0 = wp[0], w1 = wp[lpd], w2 = wp[2 * lpd], w3 = wp[3 * lpd];
+          const float d0 = dp[0], d1 = dp[lpd], d2 = dp[2 * lpd], d3 = dp[3 * lpd];
+          sd += w0 * d0;
+          s1 += w1 * d1;
+          sd += w2 * d2;
+          s1 += w3 * d3;
+          wp += 4 * lpd;
+          dp += 4 * lpd;
+        }
+        for (; k < n; ++k) {
+          sd += wp[0] * dp[0];
+          wp += lpd;
+          dp += lpd;
+        }
+        sd += s1;
       }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) s += wv[u] * dv[u];
+      for (int m = 1; m < lpd; m <<= 1) sd += __shfl_xor(sd, m, 64);
+      if (q < nh && part == 0) {
+        const float h = hs[q];
+        D1[(size_t)(p0 + p) * lda1 + j] = sd * (h * (1.0f - h));
+      }
     }
-    const float h = hs[p * H + j];
-    D1[(size_t)(p0 + p) * lda1 + j] = s * (h * (1.0f - h));
   }
   // block error partial, fixed order
   const int lane = tid & 63, wave = tid >> 6;
@@ -273,27 +307,27 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     for (int pc = 0; pc < rows; pc += ch) {
       const int cn = min(ch, rows - pc);
       const f32x4* src = reinterpret_cast<const f32x4*>(D2 + (size_t)pc * ldd2);
-      for (int i0 = tid; i0 < cn * q4; i0 += 4 * kTU) {
+      // the chunk's delta rows and activation columns are loaded in one round
+      const int nd = cn * q4, na = cn * nj;
+      for (int i0 = tid; i0 < max(nd, na); i0 += 4 * kTU) {
         f32x4 v[4];
+        float av[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = src[min(i0 + u * kTU, cn * q4 - 1)];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (i0 + u * kTU < cn * q4) reinterpret_cast<f32x4*>(d2s)[i0 + u * kTU] = v[u];
-      }
-      for (int i0 = tid; i0 < cn * nj; i0 += 4 * kTU) {
-        float v[4];
+        for (int u = 0; u < 4; ++u) v[u] = src[min(i0 + u * kTU, nd - 1)];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int i = min(i0 + u * kTU, cn * nj - 1);
+          const int i = min(i0 + u * kTU, na - 1);
           int p = 0, jj = 0;
           divmod(i, nj, inv_nj, p, jj);
           const float a = A1[(size_t)(pc + p) * lda1 + min(jlo + jj, H - 1)];
-          v[u] = jlo + jj < H ? a : 1.f;
+          av[u] = jlo + jj < H ? a : 1.f;
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          if (i0 + u * kTU < cn * nj) a1s[i0 + u * kTU] = v[u];
+          if (i0 + u * kTU < nd) reinterpret_cast<f32x4*>(d2s)[i0 + u * kTU] = v[u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kTU < na) a1s[i0 + u * kTU] = av[u];
       }
       __syncthreads();
       const int s0 = cn * wave / kWU, s1 = cn * (wave + 1) / kWU;
