@@ -306,10 +306,10 @@ int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, doubl
   const int n0 = net->n[0], H = net->n[1], O = net->n[2];
   BP_LAUNCH(net, BP_K_FUSED_FB,
             bpk::small_fwdbwd(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], n0, H, wl(net, 1), net->ldw[1], O,
-                              T, net->act[1], net->lda[1], net->del[1], net->del[2], net->lda[2], sse_part,
+                              T, net->splitk, net->del[1], net->lda[1], net->del[2], net->lda[2], sse_part,
                               net->sig_tab));
   BP_LAUNCH(net, BP_K_FUSED_UPD,
-            bpk::small_update(s, in.act, in.n_active, rows, net->act[1], net->del[1], net->lda[1], net->del[2],
+            bpk::small_update(s, in.act, in.n_active, rows, net->splitk, net->del[1], net->lda[1], net->del[2],
                               net->lda[2], wl(net, 0), vl(net, 0), net->ldw[0], n0, H, wl(net, 1), vl(net, 1),
                               net->ldw[1], O, lr, mom, net->fault_limit, net->faults));
   return BP_OK;
@@ -360,8 +360,10 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
   // every batch but the last has rows_max rows
   const int64_t nb = (n + batch - 1) / batch;
   const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
-  int rc = ensure_workspace(net, rows_max, 0,
-                            std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows)));
+  size_t sk = std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows));
+  if (use_small(net, in))   // the fused path's transposed activations take the split-K workspace
+    sk = std::max(sk, bpk::small_scratch_floats((int)rows_max, net->n[1]));
+  int rc = ensure_workspace(net, rows_max, 0, sk);
   if (rc) return rc;
   // exact number of error partials
   const size_t need = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +

@@ -12,14 +12,16 @@
 //                  error; hidden deltas from the same W1 (before its update).
 //                  Each block handles P patterns.
 //   small_update   the summed changes of both layers and the momentum update
-//                  of every weight.  Each output element is summed over the
-//                  batch in pattern order by a fixed set of lanes, partial
-//                  sums combined in a fixed order: no atomics, run-to-run
+//                  of every weight.  Each element is summed over the batch
+//                  in pattern order by a fixed set of lanes, partial sums
+//                  combined in a fixed order: no atomics, run-to-run
 //                  identical.
 //
 // Arithmetic per element is the method's (sections 3 and 6.2.1); only the
 // grouping of the work differs from the generic path.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "bp_device.h"
 #include "bp_internal.h"
@@ -31,7 +33,6 @@ constexpr int kT = 1024;       // threads per forward/backward block (16 waves)
 constexpr int kTU = 1024;      // threads per update block (16 waves)
 constexpr int kWU = kTU / 64;
 constexpr int kMaxP = 8;       // patterns per forward/backward block
-constexpr int kStageFloats = 32768;   // LDS floats the update blocks stage batch chunks in
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -43,11 +44,46 @@ __device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int&
   rem = q - quo * d;
 }
 
-// Dynamic LDS of small_fwdbwd: W1 as (H + 1) x (O + 1) (odd row stride so
-// that column walks by consecutive hidden units hit distinct banks), the
-// hidden activations [P][H], the output deltas [P][O], the targets [P][O]
-// and the active indices [P][n_active] of the block's patterns.
-//
+// Sum over aligned groups of 2^lg adjacent lanes (lg <= 4) by DPP lane moves
+// inside each row of 16 lanes: lanes i ^ 1, lanes i ^ 2, then the mirror
+// images within 8 and within 16 lanes.  Every lane of a group ends with the
+// same value (each step adds two equal-shaped partial sums, and float
+// addition is commutative).  All lanes of the wave must make the call.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), kCtrl, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float group_sum(float v, int lg) {
+  if (lg >= 1) v += dpp_move<0xB1>(v);    // quad_perm [1, 0, 3, 2]
+  if (lg >= 2) v += dpp_move<0x4E>(v);    // quad_perm [2, 3, 0, 1]
+  if (lg >= 3) v += dpp_move<0x141>(v);   // row_half_mirror
+  if (lg >= 4) v += dpp_move<0x140>(v);   // row_mirror
+  return v;
+}
+
+// Padded extents of the LDS copies: hidden units to a multiple of 128 and
+// outputs to a multiple of 32, so that every lane of the output and delta
+// sums reads a fixed multiple of 8 (resp. 4) entries, the padding being zero.
+// W1's row stride S1 = Op + 4 is 4 modulo 64: the lanes of an output sum
+// (consecutive hidden units, a few adjacent outputs) and of a delta sum
+// (consecutive hidden units, adjacent outputs) fall on distinct banks.
+__host__ __device__ __forceinline__ int small_hp(int H) { return (H + 127) / 128 * 128; }
+__host__ __device__ __forceinline__ int small_op(int O) { return (O + 31) / 32 * 32; }
+
+// Dynamic LDS of small_fwdbwd (floats unless noted):
+//   w1s  Hp x S1      W1 rows 0 .. H-1 (rows H .. Hp-1, columns O .. Op-1 zero)
+//   b1s  Op           the bias row of W1
+//   hs   P x Hp       hidden activations (units H .. Hp-1 zero)
+//   d2s  P x Op       output deltas (outputs O .. Op-1 zero)
+//   ts   P x O        targets
+//   idx  P x n_active active input indices (int)
+__host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H, int O, int n_active) {
+  const int Hp = small_hp(H), Op = small_op(O);
+  return (size_t)Hp * (Op + 4) + Op + (size_t)P * (Hp + Op + O + n_active);
+}
+
 // 1024 threads (16 waves, four per SIMD) per block of P patterns: every
 // phase is spread over all of them, so each lane's chain of dependent LDS
 // reads is short and the waves of a SIMD hide each other's latencies.
@@ -55,11 +91,14 @@ __device__ __forceinline__ void divmod(int q, int d, float inv_d, int& quo, int&
 //   gather    one (pattern, hidden unit) pair per thread: bias + the active
 //             rows of W0, in index order -> sigma;
 //   output    each output (p, c) summed by 2^lg adjacent lanes, lane k over
-//             the hidden units k, k + 2^lg, ..., combined by a butterfly;
+//             the hidden units k, k + 2^lg, ..., combined by group_sum;
 //   deltas    each hidden delta (p, j) summed by 2^lq adjacent lanes, lane k
-//             over the outputs k, k + 2^lq, ..., combined by a butterfly.
-// The strided shares walk LDS by pointer increments, with no clamped or
-// guarded reads in the inner loops.
+//             over the outputs k, k + 2^lq, ..., combined by group_sum.
+// Every lane reads its whole share of an output or delta sum in one round of
+// independent LDS reads (the padding makes the count fixed).  For the
+// update, hidden activations go out transposed (A1T[j][p], so that the
+// change of a W1 row reads one contiguous row), output deltas as rows of D2
+// and hidden deltas as rows of D1.
 // P (patterns per block) and TAB (table sigmoid) are template parameters so
 // that each instantiation holds only the code it runs: these kernels are
 // short enough that instruction-cache misses at launch are a visible part of
@@ -68,15 +107,17 @@ template <int P, bool TAB>
 __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                           const float* __restrict__ W0, int ldw0, int n0,
                                                           int H, const float* __restrict__ W1, int ldw1, int O,
-                                                          const float* __restrict__ T, float* A1, int lda1,
-                                                          float* D1, float* D2, int ldd2, double* sse_part,
-                                                          const float* __restrict__ tab) {
+                                                          const float* __restrict__ T, float* A1T, int ldt,
+                                                          float* D1, int ldd1, float* D2, int ldd2,
+                                                          double* sse_part, const float* __restrict__ tab) {
   extern __shared__ float smem[];
-  const int S1 = O + 1;
-  float* w1s = smem;                                         // (H + 1) x S1
-  float* hs = w1s + (H + 1) * S1;                            // P x H
-  float* d2s = hs + P * H;                                   // P x O
-  float* ts = d2s + P * O;                                   // P x O
+  const int Hp = small_hp(H), Op = small_op(O), S1 = Op + 4;
+  const int lhp = Hp == 128 ? 7 : 8;                         // log2(Hp)
+  float* w1s = smem;                                         // Hp x S1
+  float* b1s = w1s + Hp * S1;                                // Op
+  float* hs = b1s + Op;                                      // P x Hp
+  float* d2s = hs + P * Hp;                                  // P x Op
+  float* ts = d2s + P * Op;                                  // P x O
   int* idx = reinterpret_cast<int*>(ts + P * O);             // P x n_active
   __shared__ float red[kT / 64];
 
@@ -85,151 +126,152 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   const int np = min(P, rows - p0);
   const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
-  // round 1 (np * n_active <= 256 and np * O <= 512 <= kT by the path's
-  // limits).  Every load reads a clamped, valid address and the predicate
-  // only selects the value: no load sits behind a branch, so all are in
-  // flight together.  (Rows of act and of T are contiguous.)
+  // round 1 (np * n_active <= 256, np * O <= 512 and P * Op <= 512 <= kT by
+  // the path's limits).  Every load reads a clamped, valid address and the
+  // predicate only selects the value: no load sits behind a branch, so all
+  // are in flight together.  (Rows of act and of T are contiguous.)
   {
     const int ni = np * n_active, nt = np * O;
     const int iv = act[(size_t)p0 * n_active + min(tid, ni - 1)];
     const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
-    // W1: lane column c = tid % cw, rows tid / cw + k (kT / cw)
-    const int cw = O <= 32 ? 32 : 64, rpp = kT / cw;
-    const int c = tid & (cw - 1), jt = tid / cw;
-    for (int k0 = 0; k0 * rpp <= H; k0 += 4) {
+    const float bv = W1[(size_t)H * ldw1 + min(tid, O - 1)];
+    // W1: lane column c = tid % Op, rows tid / Op + k (kT / Op)
+    const int rpp = kT / Op;
+    const int c = tid & (Op - 1), jt = tid / Op;
+    for (int k0 = 0; k0 * rpp < Hp; k0 += 4) {
       float v[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int j = jt + (k0 + u) * rpp;
-        v[u] = W1[(size_t)min(j, H) * ldw1 + min(c, O - 1)];
+        v[u] = W1[(size_t)min(j, H - 1) * ldw1 + min(c, O - 1)];
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int j = jt + (k0 + u) * rpp;
-        if (c < O && j <= H) w1s[j * S1 + c] = v[u];
+        if (j < Hp) w1s[j * S1 + c] = (j < H && c < O) ? v[u] : 0.f;
       }
     }
+    if (tid < Op) b1s[tid] = tid < O ? bv : 0.f;
+    if (tid < P * Op && (tid & (Op - 1)) >= O) d2s[tid] = 0.f;
     if (tid < ni) idx[tid] = iv;
     if (tid < nt) ts[tid] = t0;
   }
   __syncthreads();
-  // gather: net = bias + the active rows of W0 (in index order)
-  for (int t = tid; t < np * H; t += kT) {
-    int p = 0, j = 0;
-    divmod(t, H, inv_H, p, j);
+  // gather: net = bias + the active rows of W0 (in index order); units
+  // H .. Hp-1 get 0
+  for (int t = tid; t < np * Hp; t += kT) {
+    const int p = t >> lhp, j = t & (Hp - 1), jc = min(j, H - 1);
     const int* ip = idx + p * n_active;
     float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = W0[(size_t)ip[min(u, n_active - 1)] * ldw0 + j];
-    float net = W0[(size_t)n0 * ldw0 + j];
+    for (int u = 0; u < 8; ++u) v[u] = W0[(size_t)ip[min(u, n_active - 1)] * ldw0 + jc];
+    float net = W0[(size_t)n0 * ldw0 + jc];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
       if (u < n_active) net += v[u];
-    for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + j];
+    for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + jc];
     const float h = TAB ? logistic_table(net, tab) : logistic(net);
-    hs[t] = h;
-    A1[(size_t)(p0 + p) * lda1 + j] = h;
+    hs[t] = j < H ? h : 0.f;
+    if (j < H) A1T[(size_t)j * ldt + p0 + p] = h;
   }
   __syncthreads();
-  // Output layer, output deltas and squared error.  Each output (p, c) is
-  // computed by `lpo` adjacent lanes; the lanes' partial sums are combined by
-  // a butterfly, which gives every lane of the group the same (commutative)
-  // sum.
+  // Output layer, output deltas and squared error.
   float sse = 0.f;
   {
     const int nout = np * O;
     int lg = 4;
     while (lg > 0 && (nout << lg) > kT) --lg;
-    const int lpo = 1 << lg;
+    const int lpo = 1 << lg, n = Hp >> lg;              // n: multiple of 8
+    const int ws = lpo * S1;
     for (int t0 = 0; t0 < (nout << lg); t0 += kT) {
       const int t = t0 + tid;
       const int q = t >> lg, part = t & (lpo - 1);
       int p = 0, c = 0;
-      divmod(q, O, inv_O, p, c);
-      float z = 0.f;
-      if (q < nout) {
-        const float* hp = hs + p * H + part;           // units part, part + lpo, ...
-        const float* wp = w1s + part * S1 + c;
-        const int n = (H - part + lpo - 1) >> lg;       // units of this lane
-        const int ws = lpo * S1;
-        float z1 = 0.f;
-        int k = 0;
-        for (; k + 4 <= n; k += 4) {
-          const float h0 = hp[0], h1 = hp[lpo], h2 = hp[2 * lpo], h3 = hp[3 * lpo];
-          const float w0 = wp[0], w1 = wp[ws], w2 = wp[2 * ws], w3 = wp[3 * ws];
-          z += h0 * w0;
-          z1 += h1 * w1;
-          z += h2 * w2;
-          z1 += h3 * w3;
-          hp += 4 * lpo;
-          wp += 4 * ws;
+      divmod(min(q, nout - 1), O, inv_O, p, c);
+      const float* hp = hs + p * Hp + part;             // units part, part + lpo, ...
+      const float* wp = w1s + part * S1 + c;
+      float z0 = 0.f, z1 = 0.f;
+      for (int k = 0; k < n; k += 8) {
+        float h[8], w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          h[u] = hp[u * lpo];
+          w[u] = wp[u * ws];
         }
-        for (; k < n; ++k) {
-          z += hp[0] * wp[0];
-          hp += lpo;
-          wp += ws;
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          z0 += h[u] * w[u];
+          z1 += h[u + 1] * w[u + 1];
         }
-        z += z1;
+        hp += 8 * lpo;
+        wp += 8 * ws;
       }
-      for (int m = 1; m < lpo; m <<= 1) z += __shfl_xor(z, m, 64);
+      const float z = group_sum(z0 + z1, lg);
       if (q < nout && part == 0) {
-        const float zo = w1s[H * S1 + c] + z;
+        const float zo = b1s[c] + z;
         const float y = TAB ? logistic_table(zo, tab) : logistic(zo);
         const float e = ts[q] - y;
         sse += e * e;
         const float d = e * y * (1.0f - y);
-        d2s[q] = d;
+        d2s[p * Op + c] = d;
         D2[(size_t)(p0 + p) * ldd2 + c] = d;
       }
     }
   }
   __syncthreads();
-  // hidden deltas (W1 before its update, bias row excluded): each (p, j) by
-  // `lpd` adjacent lanes, each summing a contiguous share of the outputs
+  // hidden deltas (W1 before its update, bias row excluded)
   {
     const int nh = np * H;
     int lq = 3;
     while (lq > 0 && (nh << lq) > kT) --lq;
-    const int lpd = 1 << lq;
+    const int lpd = 1 << lq, n = Op >> lq;              // n: multiple of 4
     for (int t0 = 0; t0 < (nh << lq); t0 += kT) {
       const int t = t0 + tid;
       const int q = t >> lq, part = t & (lpd - 1);
       int p = 0, j = 0;
-      divmod(q, H, inv_H, p, j);
-      float sd = 0.f;
-      if (q < nh) {
-        const float* wp = w1s + j * S1 + part;         // outputs part, part + lpd, ...
-        const float* dp = d2s + p * O + part;
-        const int n = (O - part + lpd - 1) >> lq;
-        float s1 = 0.f;
-        int k = 0;
-        for (; k + 4 <= n; k += 4) {
-          const float w0 = wp[0], w1 = wp[lpd], w2 = wp[2 * lpd], w3 = wp[3 * lpd];
-          const float d0 = dp[0], d1 = dp[lpd], d2 = dp[2 * lpd], d3 = dp[3 * lpd];
-          sd += w0 * d0;
-          s1 += w1 * d1;
-          sd += w2 * d2;
-          s1 += w3 * d3;
-          wp += 4 * lpd;
-          dp += 4 * lpd;
+      divmod(min(q, nh - 1), H, inv_H, p, j);
+      const float* wp = w1s + j * S1 + part;            // outputs part, part + lpd, ...
+      const float* dp = d2s + p * Op + part;
+      float s0 = 0.f, s1 = 0.f;
+      int k = 0;
+      for (; k + 8 <= n; k += 8) {
+        float w[8], d[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          w[u] = wp[u * lpd];
+          d[u] = dp[u * lpd];
         }
-        for (; k < n; ++k) {
-          sd += wp[0] * dp[0];
-          wp += lpd;
-          dp += lpd;
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          s0 += w[u] * d[u];
+          s1 += w[u + 1] * d[u + 1];
         }
-        sd += s1;
+        wp += 8 * lpd;
+        dp += 8 * lpd;
       }
-      for (int m = 1; m < lpd; m <<= 1) sd += __shfl_xor(sd, m, 64);
+      if (k < n) {
+        float w[4], d[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          w[u] = wp[u * lpd];
+          d[u] = dp[u * lpd];
+        }
+        s0 += w[0] * d[0];
+        s1 += w[1] * d[1];
+        s0 += w[2] * d[2];
+        s1 += w[3] * d[3];
+      }
+      const float sd = group_sum(s0 + s1, lq);
       if (q < nh && part == 0) {
-        const float h = hs[q];
-        D1[(size_t)(p0 + p) * lda1 + j] = sd * (h * (1.0f - h));
+        const float h = hs[p * Hp + j];
+        D1[(size_t)(p0 + p) * ldd1 + j] = sd * (h * (1.0f - h));
       }
     }
   }
-  // block error partial, fixed order
+  // block error partial, fixed order: rows of 16 lanes, then the four rows
   const int lane = tid & 63, wave = tid >> 6;
-  for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+  sse = group_sum(sse, 4);
+  sse = (__shfl(sse, 0, 64) + __shfl(sse, 16, 64)) + (__shfl(sse, 32, 64) + __shfl(sse, 48, 64));
   if (lane == 0) red[wave] = sse;
   __syncthreads();
   if (tid == 0) {
@@ -239,56 +281,69 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   }
 }
 
+// Patterns staged per chunk by the update's W1-tile blocks (D2 rows of
+// Op / 4 float4 plus one float4 of activations each): 4096 float4 of D2.
+__host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 / (small_op(O) / 4); }
+
 // 1024 threads = 16 waves per block.  The weight and momentum a lane updates
-// are loaded at the start, overlapping the sums.  Batch sums over patterns
-// run in chunks of `ch` patterns staged in LDS with wide coalesced loads; wave
-// w adds its sixteenth of each chunk in pattern order, and the 16 wave
-// partials are combined in wave order.
-// Blocks [0, nA): W1 elements o = 64 b + lane (row o / O, column o % O):
-//   sum_p A1[p][j] D2[p][c] (the bias row H takes 1 for A1).
-// Blocks [nA, nA + n0): row r of W0: the delta rows of the patterns whose
+// are loaded at the start, overlapping the sums.  Batch sums run over chunks
+// of `ch` patterns staged in LDS by one round of coalesced loads.
+// Blocks [0, nT): rows j0 .. j0+3 of W1 (j0 = 4 b; row H is the bias row,
+//   activation 1), all O columns: G[j][c] = sum_p A1[p][j] D2[p][c].  Waves
+//   0-7 compute: lane (sub, g) holds the 4 x 4 tile of rows j0 .. j0+3 and
+//   columns 4 sub .. 4 sub + 3 over the patterns g, g + ng, g + 2 ng, ... in
+//   order (ng = 512 / (Op / 4) lane groups); the group sums are then added
+//   through LDS in a fixed tree.
+// Blocks [nT, nT + n0): row r of W0: the delta rows of the patterns whose
 //   active list holds r, in pattern order (ballot compaction of 1024
 //   patterns at a time); wave w owns the column strip (w % 4) and quarter
 //   (w / 4) of each compacted list.
-// Blocks [nA + n0, nA + n0 + nS): the bias row of W0, 64 columns per block:
-//   sum_p D1[p][j].
+// Blocks [nT + n0, nT + n0 + nS): the bias row of W0, 32 columns per block:
+//   sum_p D1[p][j], the half-wave h of wave w adding the (2 w + h)-th of 32
+//   slices of each chunk in pattern order, the 32 slice sums combined in
+//   slice order.
 // CHECK: the range check of the summed changes (limit > 0).
 template <bool CHECK>
 __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __restrict__ act, int n_active, int rows,
-                                                           const float* __restrict__ A1, const float* __restrict__ D1,
-                                                           int lda1, const float* __restrict__ D2, int ldd2,
-                                                           float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                                                           float* V1, int ldw1, int O, int nA, int ch, float lr,
-                                                           float mom, float limit, unsigned long long* faults) {
-  extern __shared__ float stage[];
+                                                           const float* __restrict__ A1T, int ldt,
+                                                           const float* __restrict__ D1, int ldd1,
+                                                           const float* __restrict__ D2, int ldd2, float* W0,
+                                                           float* V0, int ldw0, int n0, int H, float* W1, float* V1,
+                                                           int ldw1, int O, int nT, int ch, float lr, float mom,
+                                                           float limit, unsigned long long* faults) {
+  extern __shared__ f32x4 stage[];
   __shared__ float part[kWU][64];
+  __shared__ float tile_sum[256];
   __shared__ int list[kTU];
   __shared__ int wave_cnt[kWU];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
+  const int Op = small_op(O), o4 = Op >> 2;
 
   float* Wt;        // weight row this block updates
   float* Vt;
-  int col, ncol;    // lane's column in that row, row length
-  int jrow = 0;     // W1 blocks: the lane's row
-  if (b < nA) {
-    const int o = b * 64 + lane;
-    divmod(o, O, 1.0f / (float)O, jrow, col);
-    Wt = W1 + (size_t)jrow * ldw1;
-    Vt = V1 + (size_t)jrow * ldw1;
-    ncol = o < (H + 1) * O ? O : 0;
-  } else if (b < nA + n0) {
-    Wt = W0 + (size_t)(b - nA) * ldw0;
-    Vt = V0 + (size_t)(b - nA) * ldw0;
+  int col, ncol;    // thread's column in that row, row length
+  bool owner;
+  if (b < nT) {
+    const int jj = tid / Op, j = b * 4 + jj;
+    col = tid & (Op - 1);
+    Wt = W1 + (size_t)min(j, H) * ldw1;
+    Vt = V1 + (size_t)min(j, H) * ldw1;
+    ncol = j <= H ? O : 0;
+    owner = tid < 4 * Op;                            // whole waves
+  } else if (b < nT + n0) {
+    Wt = W0 + (size_t)(b - nT) * ldw0;
+    Vt = V0 + (size_t)(b - nT) * ldw0;
     col = (wave & 3) * 64 + lane;
     ncol = H;
+    owner = wave < 4;
   } else {
     Wt = W0 + (size_t)n0 * ldw0;
     Vt = V0 + (size_t)n0 * ldw0;
-    col = (b - nA - n0) * 64 + lane;
+    col = lane < 32 ? (b - nT - n0) * 32 + lane : H;
     ncol = H;
+    owner = wave == 0;
   }
-  const bool owner = (b < nA || b >= nA + n0) ? (wave == 0) : (wave < 4);
   const bool live = col < ncol;
   float w_old = 0.f, v_old = 0.f;
   if (owner && live) {
@@ -297,65 +352,99 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
   }
 
   float g = 0.f;
-  if (b < nA) {
-    // rows jlo .. jhi of W1 are touched by this block
-    const int jlo = (b * 64) / O, jhi = min(H, (b * 64 + 63) / O), nj = jhi - jlo + 1;
-    const float inv_nj = 1.0f / (float)nj;
-    const int q4 = ldd2 >> 2;                       // float4 per D2 row (ldd2 % 4 == 0)
-    float* d2s = stage;                             // [ch][ldd2]
-    float* a1s = stage + ch * ldd2;                 // [ch][nj]
+  if (b < nT) {
+    const int j0 = b * 4;
+    const int q4 = ldd2 >> 2;                        // float4 per D2 row (ldd2 % 4 == 0)
+    const int lo4 = o4 == 8 ? 3 : 4;                 // log2(o4)
+    f32x4* d2s = stage;                              // [ch][o4], columns past ldd2 zero
+    float* a1s = reinterpret_cast<float*>(stage + ch * o4);   // [ch][4]
+    const f32x4* d2g = reinterpret_cast<const f32x4*>(D2);
+    const int sub = tid & (o4 - 1), grp = tid >> lo4, ng = 512 >> lo4;
+    float acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.f;
     for (int pc = 0; pc < rows; pc += ch) {
       const int cn = min(ch, rows - pc);
-      const f32x4* src = reinterpret_cast<const f32x4*>(D2 + (size_t)pc * ldd2);
-      // the chunk's delta rows and activation columns are loaded in one round
-      const int nd = cn * q4, na = cn * nj;
-      for (int i0 = tid; i0 < max(nd, na); i0 += 4 * kTU) {
+      // one round: ch * o4 = 4096 float4 of D2 (4 per thread) and 4 cn <= 2048
+      // activations (2 per thread), clamped addresses, values selected
+      {
+        const int nd = cn * o4, na = 4 * cn;
         f32x4 v[4];
-        float av[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = src[min(i0 + u * kTU, nd - 1)];
+        float av[2];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int i = min(i0 + u * kTU, na - 1);
-          int p = 0, jj = 0;
-          divmod(i, nj, inv_nj, p, jj);
-          const float a = A1[(size_t)(pc + p) * lda1 + min(jlo + jj, H - 1)];
-          av[u] = jlo + jj < H ? a : 1.f;
+          const int i = min(tid + u * kTU, nd - 1);
+          const int p = i >> lo4, k = i & (o4 - 1);
+          v[u] = d2g[(size_t)(pc + p) * q4 + min(k, q4 - 1)];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (i0 + u * kTU < nd) reinterpret_cast<f32x4*>(d2s)[i0 + u * kTU] = v[u];
+        for (int u = 0; u < 2; ++u) {
+          const int i = min(tid + u * kTU, na - 1);
+          const int p = i >> 2, j = j0 + (i & 3);
+          const float a = A1T[(size_t)min(j, H - 1) * ldt + pc + p];
+          av[u] = j < H ? a : (j == H ? 1.0f : 0.f);
+        }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (i0 + u * kTU < na) a1s[i0 + u * kTU] = av[u];
+        for (int u = 0; u < 4; ++u) {
+          const int i = tid + u * kTU;
+          if (i < nd) d2s[i] = (i & (o4 - 1)) < q4 ? v[u] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int i = tid + u * kTU;
+          if (i < na) a1s[i] = av[u];
+        }
       }
       __syncthreads();
-      const int s0 = cn * wave / kWU, s1 = cn * (wave + 1) / kWU;
-      if (live) {
-        const int jj = jrow - jlo;
-        for (int p = s0; p < s1; p += 8) {
-          float av[8], dv[8];
+      if (tid < 512) {
+        for (int p = grp; p < cn; p += 4 * ng) {
+          f32x4 a[4], d[4];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int pp = min(p + u, s1 - 1);
-            av[u] = a1s[pp * nj + jj];
-            dv[u] = d2s[pp * ldd2 + col];
+          for (int u = 0; u < 4; ++u) {
+            const int pp = min(p + u * ng, cn - 1);
+            a[u] = reinterpret_cast<const f32x4*>(a1s)[pp];
+            d[u] = d2s[pp * o4 + sub];
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (p + u < s1) g += av[u] * dv[u];
+          for (int u = 0; u < 4; ++u)
+            if (p + u * ng < cn) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) acc[r * 4 + q] += a[u][r] * d[u][q];
+            }
         }
       }
       __syncthreads();
     }
-    part[wave][lane] = g;
-    __syncthreads();
-    if (owner) {
-      g = part[0][lane];
-      for (int w = 1; w < kWU; ++w) g += part[w][lane];
+    // the lane groups' tiles through LDS: group grp's 16 o4 sums at
+    // accs[grp * S + i * Op + 4 sub + q] (acc[4 i + q]; row stride S = 16 o4
+    // + 8 floats keeps both the writes and the strided reads below free of
+    // bank conflicts).  Element el = i * Op + 4 sub + q is summed by
+    // tpe = 1024 / (16 o4) adjacent threads, thread s over the 8 groups s,
+    // s + tpe, ..., the partial sums combined by group_sum.
+    const int S4 = 4 * o4 + 2;                           // row stride in float4
+    if (tid < 512) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        stage[grp * S4 + i * o4 + sub] = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
     }
-  } else if (b < nA + n0) {
-    const int r = b - nA;
+    __syncthreads();
+    {
+      const int lt = 6 - lo4, tpe = 1 << lt;             // 8 (o4 = 8) or 4 (o4 = 16)
+      const int el = tid >> lt, sl = tid & (tpe - 1);
+      const float* src = reinterpret_cast<const float*>(stage) + el;
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = src[(sl + tpe * u) * (4 * S4)];   // ng = 8 tpe groups
+      float x = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7])));
+      x = group_sum(x, lt);
+      if (sl == 0) tile_sum[el] = x;
+    }
+    __syncthreads();
+    if (owner) g = tile_sum[tid];                       // tid = jj Op + col
+  } else if (b < nT + n0) {
+    const int r = b - nT;
     const int quarter = wave >> 2;
     for (int pc = 0; pc < rows; pc += kTU) {
       const int p = pc + tid;
@@ -388,7 +477,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         for (int q = q0; q < q1; q += 16) {
           float v[16];
 #pragma unroll
-          for (int u = 0; u < 16; ++u) v[u] = D1[(size_t)list[min(q + u, q1 - 1)] * lda1 + col];
+          for (int u = 0; u < 16; ++u) v[u] = D1[(size_t)list[min(q + u, q1 - 1)] * ldd1 + col];
 #pragma unroll
           for (int u = 0; u < 16; ++u)
             if (q + u < q1) s += v[u];
@@ -401,43 +490,40 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       __syncthreads();
     }
   } else {
-    // bias row of W0: columns c0 .. c0 + 63 of D1, staged as float4 (a D1
-    // row is lda1 floats, lda1 % 4 == 0; lanes past H are never summed)
-    const int c0 = (b - nA - n0) * 64;
-    float* d1s = stage;                             // [ch][64]
-    for (int pc = 0; pc < rows; pc += ch) {
-      const int cn = min(ch, rows - pc);
-      for (int i0 = tid; i0 < cn * 16; i0 += 8 * kTU) {
-        f32x4 v[8];
+    // bias row of W0: columns c0 .. c0 + 31 of D1, staged as float4 (a D1
+    // row is ldd1 floats, ldd1 % 4 == 0; columns past H are never summed),
+    // 512 patterns per chunk
+    const int c0 = (b - nT - n0) * 32, c = lane & 31, h = lane >> 5;
+    f32x4* d1s = stage;                              // [512][8]
+    for (int pc = 0; pc < rows; pc += 512) {
+      const int cn = min(512, rows - pc), nd = cn * 8;
+      f32x4 v[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = min(i0 + u * kTU, cn * 16 - 1);
-          const int cc = min(c0 + (i & 15) * 4, lda1 - 4);
-          v[u] = *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 4)) * lda1 + cc);
-        }
+      for (int u = 0; u < 4; ++u) {
+        const int i = min(tid + u * kTU, nd - 1);
+        const int cc = min(c0 + (i & 7) * 4, ldd1 - 4);
+        v[u] = *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 3)) * ldd1 + cc);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (tid + u * kTU < nd) d1s[tid + u * kTU] = v[u];
+      __syncthreads();
+      const int sl = 2 * wave + h, s0 = cn * sl / 32, s1 = cn * (sl + 1) / 32;
+      const float* col_s = reinterpret_cast<const float*>(d1s) + c;
+      float sum = 0.f;
+      for (int p = s0; p < s1; p += 8) {
+        float dv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) dv[u] = col_s[min(p + u, s1 - 1) * 32];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-          if (i0 + u * kTU < cn * 16) reinterpret_cast<f32x4*>(d1s)[i0 + u * kTU] = v[u];
+          if (p + u < s1) sum += dv[u];
       }
+      part[wave][lane] = sum;
       __syncthreads();
-      const int s0 = cn * wave / kWU, s1 = cn * (wave + 1) / kWU;
-      if (live) {
-        for (int p = s0; p < s1; p += 8) {
-          float dv[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) dv[u] = d1s[min(p + u, s1 - 1) * 64 + lane];
-#pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (p + u < s1) g += dv[u];
-        }
-      }
+      if (owner && lane < 32)
+        for (int w = 0; w < kWU; ++w) g = (g + part[w][lane]) + part[w][lane + 32];
       __syncthreads();
-    }
-    part[wave][lane] = g;
-    __syncthreads();
-    if (owner) {
-      g = part[0][lane];
-      for (int w = 1; w < kWU; ++w) g += part[w][lane];
     }
   }
   if (owner) {   // whole waves
@@ -471,51 +557,48 @@ int small_fwdbwd_blocks(int rows) {
   return (rows + P - 1) / P;
 }
 
+size_t small_scratch_floats(int rows, int H) { return rows > 0 ? (size_t)H * rows : 0; }
+
 template <bool TAB>
 hipError_t launch_fwdbwd(hipStream_t s, int P, int nb, size_t lds, const int32_t* act, int n_active, int rows,
                          const float* W0, int ldw0, int n0, int H, const float* W1, int ldw1, int O, const float* T,
-                         float* A1, int lda1, float* D1, float* D2, int ldd2, double* sse_part, const float* tab) {
+                         float* A1T, float* D1, int ldd1, float* D2, int ldd2, double* sse_part, const float* tab) {
   switch (P) {
-    case 1: return launch_kernel(small_fwdbwd_kernel<1, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
-    case 2: return launch_kernel(small_fwdbwd_kernel<2, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
-    case 4: return launch_kernel(small_fwdbwd_kernel<4, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
-    default: return launch_kernel(small_fwdbwd_kernel<8, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2, ldd2, sse_part, tab);
+    case 1: return launch_kernel(small_fwdbwd_kernel<1, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
+    case 2: return launch_kernel(small_fwdbwd_kernel<2, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
+    case 4: return launch_kernel(small_fwdbwd_kernel<4, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
+    default: return launch_kernel(small_fwdbwd_kernel<8, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
   }
 }
 
 hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
-                        int H, const float* W1, int ldw1, int O, const float* T, float* A1, int lda1, float* D1,
+                        int H, const float* W1, int ldw1, int O, const float* T, float* A1T, float* D1, int ldd1,
                         float* D2, int ldd2, double* sse_part, const float* tab) {
   if (rows <= 0) return hipSuccess;
   const int P = patterns_per_block(rows);
-  const size_t lds = sizeof(float) * ((size_t)(H + 1) * (O + 1) + (size_t)P * H + 2 * (size_t)P * O) +
-                     sizeof(int) * (size_t)P * n_active;
+  const size_t lds = sizeof(float) * small_fwdbwd_lds_floats(P, H, O, n_active);
   const int nb = small_fwdbwd_blocks(rows);
   if (tab)
-    return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2,
-                               ldd2, sse_part, tab);
-  return launch_fwdbwd<false>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1, lda1, D1, D2,
+    return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, D1, ldd1,
+                               D2, ldd2, sse_part, tab);
+  return launch_fwdbwd<false>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, D1, ldd1, D2,
                               ldd2, sse_part, tab);
 }
 
-hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1, const float* D1,
-                        int lda1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
+hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1T, const float* D1,
+                        int ldd1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
                         float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults) {
   if (rows <= 0) return hipSuccess;
-  const int nA = ((H + 1) * O + 63) / 64;
-  const int nS = (H + 63) / 64;
-  // patterns staged per round: the largest power of two that fits
-  // kStageFloats for both block types (>= 128 since ldd2 + njmax <= 134)
-  const int njmax = 64 / O + 2;
-  const int per = (ldd2 + njmax) > 64 ? (ldd2 + njmax) : 64;
-  int ch = 1;
-  while (ch * 2 * per <= kStageFloats) ch *= 2;
-  const size_t lds = sizeof(float) * (size_t)ch * per;
+  const int nT = (H + 1 + 3) / 4;
+  const int nS = (H + 31) / 32;
+  const int ch = small_update_chunk(O), o4 = small_op(O) / 4;
+  // tile chunks: ch (o4 + 1) float4; bias-row chunks: 512 rows of 8 float4
+  const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1), (size_t)512 * 8);
   if (limit > 0.f)
-    return launch_kernel(small_update_kernel<true>, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2,
-                         ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom, limit, faults);
-  return launch_kernel(small_update_kernel<false>, nA + n0 + nS, kTU, lds, s, act, n_active, rows, A1, D1, lda1, D2,
-                       ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nA, ch, lr, mom, limit, faults);
+    return launch_kernel(small_update_kernel<true>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1T, rows, D1,
+                         ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
+  return launch_kernel(small_update_kernel<false>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1T, rows, D1,
+                       ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
 }
 
 }  // namespace bpk
