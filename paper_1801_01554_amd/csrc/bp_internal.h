@@ -126,18 +126,18 @@ bool small_path_fits(int n0, int H, int O, int n_active);
 int small_fwdbwd_blocks(int rows);
 
 // Floats of scratch the fused path needs for a batch of `rows` patterns
-// (the hidden activations, transposed).
+// (the hidden activations in groups of four units).
 size_t small_scratch_floats(int rows, int H);
 
 // Per pattern: A1 = sigma(W0 gather + bias), Y = sigma(A1 W1 + bias1),
 // D2 = (T - Y) Y (1 - Y), D1 = (D2 W1^T) A1 (1 - A1); error partials per
-// block.  A1 is written transposed: A1T[j * rows + p].
+// block.  A1 is written in groups of four units: A1q[((j / 4) rows + p) 4 + j % 4].
 hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
-                        int H, const float* W1, int ldw1, int O, const float* T, float* A1T, float* D1, int ldd1,
+                        int H, const float* W1, int ldw1, int O, const float* T, float* A1q, float* D1, int ldd1,
                         float* D2, int ldd2, double* sse_part, const float* tab);
 
 // Summed changes of both layers over the batch and the momentum update of all weights.
-hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1T, const float* D1,
+hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1q, const float* D1,
                         int ldd1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
                         float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults);
 

@@ -73,52 +73,58 @@ __host__ __device__ __forceinline__ int small_hp(int H) { return (H + 127) / 128
 __host__ __device__ __forceinline__ int small_op(int O) { return (O + 31) / 32 * 32; }
 
 // Dynamic LDS of small_fwdbwd (floats unless noted):
-//   w1s  Hp x S1      W1 rows 0 .. H-1 (rows H .. Hp-1, columns O .. Op-1 zero)
-//   b1s  Op           the bias row of W1
-//   hs   P x Hp       hidden activations (units H .. Hp-1 zero)
-//   d2s  P x Op       output deltas (outputs O .. Op-1 zero)
-//   ts   P x O        targets
-//   idx  P x n_active active input indices (int)
+//   w1s  HP x S1      W1 rows 0 .. H-1 (rows H .. HP-1, columns O .. OP-1 zero)
+//   b1s  OP + 64      the bias row of W1
+//   hs   P x HP       hidden activations (units H .. HP-1 zero)
+//   d2s  P x OP       output deltas (outputs O .. OP-1 zero)
+//   ts   P x O + 64   targets
+//   idx  P x n_active + 64  active input indices (int)
+// (the 64 extra entries of b1s, ts and idx take the round-1 stores of the
+// lanes past the end, one entry per lane)
 __host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H, int O, int n_active) {
   const int Hp = small_hp(H), Op = small_op(O);
-  return (size_t)Hp * (Op + 4) + Op + (size_t)P * (Hp + Op + O + n_active);
+  return (size_t)Hp * (Op + 4) + Op + 64 + (size_t)P * (Hp + Op) + (size_t)P * O + 64 + (size_t)P * n_active + 64;
 }
 
-// 1024 threads (16 waves, four per SIMD) per block of P patterns: every
-// phase is spread over all of them, so each lane's chain of dependent LDS
-// reads is short and the waves of a SIMD hide each other's latencies.
-//   round 1   indices, targets and W1: independent loads, all in flight;
+// 1024 threads (16 waves, four per SIMD) per block of P patterns.  With so
+// little work per phase, the kernel is bound by instruction issue (a wave64
+// instruction takes four cycles of its SIMD) and by dependent latencies, so
+// the padded extents HP = small_hp(H) and OP = small_op(O) are template
+// parameters: every LDS read of the sums below uses a constant offset from
+// one base address, and the staging loop has a fixed trip count.
+//   round 1   indices, targets, the bias row and W1 (HP OP / 1024 elements
+//             per thread): all loads issued before any is waited on;
 //   gather    one (pattern, hidden unit) pair per thread: bias + the active
 //             rows of W0, in index order -> sigma;
-//   output    each output (p, c) summed by 2^lg adjacent lanes, lane k over
-//             the hidden units k, k + 2^lg, ..., combined by group_sum;
-//   deltas    each hidden delta (p, j) summed by 2^lq adjacent lanes, lane k
-//             over the outputs k, k + 2^lq, ..., combined by group_sum.
-// Every lane reads its whole share of an output or delta sum in one round of
-// independent LDS reads (the padding makes the count fixed).  For the
-// update, hidden activations go out transposed (A1T[j][p], so that the
-// change of a W1 row reads one contiguous row), output deltas as rows of D2
-// and hidden deltas as rows of D1.
-// P (patterns per block) and TAB (table sigmoid) are template parameters so
-// that each instantiation holds only the code it runs: these kernels are
-// short enough that instruction-cache misses at launch are a visible part of
-// their time.
-template <int P, bool TAB>
+//   output    each output (p, c) summed by 16 adjacent lanes, lane k over
+//             the hidden units k, k + 16, ..., combined by group_sum;
+//   deltas    each hidden delta (p, j) summed by 4 adjacent lanes, lane k
+//             over the outputs k, k + 4, ..., combined by group_sum.
+// For the update, hidden activations go out in groups of four units,
+// A1q[j / 4][p][j % 4] (one float4 per pattern for the four W1 rows a block
+// of the update handles), output deltas as rows of D2 and hidden deltas as
+// rows of D1.  The activations and output deltas are written after the last
+// phase: a phase that follows global stores can wait on them (a register the
+// store read is written again), so they leave the chip when nothing else
+// waits.
+template <int P, bool TAB, int HP, int OP>
 __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                           const float* __restrict__ W0, int ldw0, int n0,
                                                           int H, const float* __restrict__ W1, int ldw1, int O,
-                                                          const float* __restrict__ T, float* A1T, int ldt,
+                                                          const float* __restrict__ T, float* A1q, int ldq,
                                                           float* D1, int ldd1, float* D2, int ldd2,
                                                           double* sse_part, const float* __restrict__ tab) {
+  constexpr int S1 = OP + 4;                                 // W1 row stride, 4 modulo 64
+  constexpr int LHP = HP == 128 ? 7 : 8;
+  constexpr int NW = HP * OP / kT;                           // W1 elements staged per thread
+  constexpr int RPP = kT / OP;                               // W1 rows per staging pass
   extern __shared__ float smem[];
-  const int Hp = small_hp(H), Op = small_op(O), S1 = Op + 4;
-  const int lhp = Hp == 128 ? 7 : 8;                         // log2(Hp)
-  float* w1s = smem;                                         // Hp x S1
-  float* b1s = w1s + Hp * S1;                                // Op
-  float* hs = b1s + Op;                                      // P x Hp
-  float* d2s = hs + P * Hp;                                  // P x Op
-  float* ts = d2s + P * Op;                                  // P x O
-  int* idx = reinterpret_cast<int*>(ts + P * O);             // P x n_active
+  float* w1s = smem;                                         // HP x S1
+  float* b1s = w1s + HP * S1;                                // OP + 64
+  float* hs = b1s + OP + 64;                                 // P x HP
+  float* d2s = hs + P * HP;                                  // P x OP
+  float* ts = d2s + P * OP;                                  // P x O + 64
+  int* idx = reinterpret_cast<int*>(ts + P * O + 64);        // P x n_active + 64
   __shared__ float red[kT / 64];
 
   const int tid = threadIdx.x;
@@ -126,41 +132,38 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   const int np = min(P, rows - p0);
   const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
-  // round 1 (np * n_active <= 256, np * O <= 512 and P * Op <= 512 <= kT by
-  // the path's limits).  Every load reads a clamped, valid address and the
-  // predicate only selects the value: no load sits behind a branch, so all
-  // are in flight together.  (Rows of act and of T are contiguous.)
+  // round 1 (np * n_active <= 256, np * O <= 512 and P * OP <= 512 <= kT by
+  // the path's limits).  Every load reads a clamped, valid address and is
+  // stored to LDS unconditionally (the value selected; lanes past the end
+  // store to a spare entry of their own), so that no load is sunk behind a
+  // branch and all are in flight together.  (Rows of act and of T are
+  // contiguous.)
   {
     const int ni = np * n_active, nt = np * O;
     const int iv = act[(size_t)p0 * n_active + min(tid, ni - 1)];
     const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
     const float bv = W1[(size_t)H * ldw1 + min(tid, O - 1)];
-    // W1: lane column c = tid % Op, rows tid / Op + k (kT / Op)
-    const int rpp = kT / Op;
-    const int c = tid & (Op - 1), jt = tid / Op;
-    for (int k0 = 0; k0 * rpp < Hp; k0 += 4) {
-      float v[4];
+    const int c = tid & (OP - 1), jt = tid / OP;
+    const float* wsrc = W1 + min(c, O - 1);
+    float v[NW];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = jt + (k0 + u) * rpp;
-        v[u] = W1[(size_t)min(j, H - 1) * ldw1 + min(c, O - 1)];
-      }
+    for (int u = 0; u < NW; ++u) v[u] = wsrc[(size_t)min(jt + u * RPP, H - 1) * ldw1];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = jt + (k0 + u) * rpp;
-        if (j < Hp) w1s[j * S1 + c] = (j < H && c < O) ? v[u] : 0.f;
-      }
+    for (int u = 0; u < NW; ++u) {
+      const int j = jt + u * RPP;
+      w1s[j * S1 + c] = (j < H && c < O) ? v[u] : 0.f;
     }
-    if (tid < Op) b1s[tid] = tid < O ? bv : 0.f;
-    if (tid < P * Op && (tid & (Op - 1)) >= O) d2s[tid] = 0.f;
-    if (tid < ni) idx[tid] = iv;
-    if (tid < nt) ts[tid] = t0;
+    const int spare = tid & 63;
+    b1s[tid < OP ? tid : OP + spare] = tid < O ? bv : 0.f;
+    idx[tid < ni ? tid : P * n_active + spare] = iv;
+    ts[tid < nt ? tid : P * O + spare] = t0;
+    if (tid < P * OP && (tid & (OP - 1)) >= O) d2s[tid] = 0.f;
   }
   __syncthreads();
   // gather: net = bias + the active rows of W0 (in index order); units
-  // H .. Hp-1 get 0
-  for (int t = tid; t < np * Hp; t += kT) {
-    const int p = t >> lhp, j = t & (Hp - 1), jc = min(j, H - 1);
+  // H .. HP-1 get 0
+  for (int t = tid; t < np * HP; t += kT) {
+    const int p = t >> LHP, j = t & (HP - 1), jc = min(j, H - 1);
     const int* ip = idx + p * n_active;
     float v[8];
 #pragma unroll
@@ -172,101 +175,66 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
     for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + jc];
     const float h = TAB ? logistic_table(net, tab) : logistic(net);
     hs[t] = j < H ? h : 0.f;
-    if (j < H) A1T[(size_t)j * ldt + p0 + p] = h;
   }
   __syncthreads();
   // Output layer, output deltas and squared error.
   float sse = 0.f;
   {
-    const int nout = np * O;
-    int lg = 4;
-    while (lg > 0 && (nout << lg) > kT) --lg;
-    const int lpo = 1 << lg, n = Hp >> lg;              // n: multiple of 8
-    const int ws = lpo * S1;
-    for (int t0 = 0; t0 < (nout << lg); t0 += kT) {
-      const int t = t0 + tid;
-      const int q = t >> lg, part = t & (lpo - 1);
+    const int nout = np * O, part = tid & 15;
+    for (int q0 = 0; q0 < nout; q0 += kT / 16) {
+      const int q = q0 + (tid >> 4);
       int p = 0, c = 0;
       divmod(min(q, nout - 1), O, inv_O, p, c);
-      const float* hp = hs + p * Hp + part;             // units part, part + lpo, ...
+      const float* hp = hs + p * HP + part;             // units part, part + 16, ...
       const float* wp = w1s + part * S1 + c;
       float z0 = 0.f, z1 = 0.f;
-      for (int k = 0; k < n; k += 8) {
-        float h[8], w[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          h[u] = hp[u * lpo];
-          w[u] = wp[u * ws];
-        }
-#pragma unroll
-        for (int u = 0; u < 8; u += 2) {
-          z0 += h[u] * w[u];
-          z1 += h[u + 1] * w[u + 1];
-        }
-        hp += 8 * lpo;
-        wp += 8 * ws;
+      for (int u = 0; u < HP / 16; u += 2) {
+        z0 += hp[16 * u] * wp[16 * u * S1];
+        z1 += hp[16 * (u + 1)] * wp[16 * (u + 1) * S1];
       }
-      const float z = group_sum(z0 + z1, lg);
+      const float z = group_sum(z0 + z1, 4);
       if (q < nout && part == 0) {
         const float zo = b1s[c] + z;
         const float y = TAB ? logistic_table(zo, tab) : logistic(zo);
         const float e = ts[q] - y;
         sse += e * e;
-        const float d = e * y * (1.0f - y);
-        d2s[p * Op + c] = d;
-        D2[(size_t)(p0 + p) * ldd2 + c] = d;
+        d2s[p * OP + c] = e * y * (1.0f - y);
       }
     }
   }
   __syncthreads();
   // hidden deltas (W1 before its update, bias row excluded)
   {
-    const int nh = np * H;
-    int lq = 3;
-    while (lq > 0 && (nh << lq) > kT) --lq;
-    const int lpd = 1 << lq, n = Op >> lq;              // n: multiple of 4
-    for (int t0 = 0; t0 < (nh << lq); t0 += kT) {
-      const int t = t0 + tid;
-      const int q = t >> lq, part = t & (lpd - 1);
+    const int nh = np * H, part = tid & 3;
+    for (int q0 = 0; q0 < nh; q0 += kT / 4) {
+      const int q = q0 + (tid >> 2);
       int p = 0, j = 0;
       divmod(min(q, nh - 1), H, inv_H, p, j);
-      const float* wp = w1s + j * S1 + part;            // outputs part, part + lpd, ...
-      const float* dp = d2s + p * Op + part;
+      const float* wp = w1s + j * S1 + part;            // outputs part, part + 4, ...
+      const float* dp = d2s + p * OP + part;
       float s0 = 0.f, s1 = 0.f;
-      int k = 0;
-      for (; k + 8 <= n; k += 8) {
-        float w[8], d[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          w[u] = wp[u * lpd];
-          d[u] = dp[u * lpd];
-        }
-#pragma unroll
-        for (int u = 0; u < 8; u += 2) {
-          s0 += w[u] * d[u];
-          s1 += w[u + 1] * d[u + 1];
-        }
-        wp += 8 * lpd;
-        dp += 8 * lpd;
+      for (int u = 0; u < OP / 4; u += 2) {
+        s0 += wp[4 * u] * dp[4 * u];
+        s1 += wp[4 * (u + 1)] * dp[4 * (u + 1)];
       }
-      if (k < n) {
-        float w[4], d[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          w[u] = wp[u * lpd];
-          d[u] = dp[u * lpd];
-        }
-        s0 += w[0] * d[0];
-        s1 += w[1] * d[1];
-        s0 += w[2] * d[2];
-        s1 += w[3] * d[3];
-      }
-      const float sd = group_sum(s0 + s1, lq);
+      const float sd = group_sum(s0 + s1, 2);
       if (q < nh && part == 0) {
-        const float h = hs[p * Hp + j];
+        const float h = hs[p * HP + j];
         D1[(size_t)(p0 + p) * ldd1 + j] = sd * (h * (1.0f - h));
       }
     }
+  }
+  // activations, quad-major so that a wave writes runs of P float4
+  for (int t = tid; t < ((H + 3) >> 2) * 4 * P; t += kT) {
+    const int r = t & 3, p = (t >> 2) & (P - 1), jq = t / (4 * P), j = 4 * jq + r;
+    if (p < np && j < H) A1q[((size_t)jq * ldq + p0 + p) * 4 + r] = hs[p * HP + j];
+  }
+  for (int t = tid; t < np * O; t += kT) {
+    int p = 0, c = 0;
+    divmod(t, O, inv_O, p, c);
+    D2[(size_t)(p0 + p) * ldd2 + c] = d2s[p * OP + c];
   }
   // block error partial, fixed order: rows of 16 lanes, then the four rows
   const int lane = tid & 63, wave = tid >> 6;
@@ -305,7 +273,7 @@ __host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 
 // CHECK: the range check of the summed changes (limit > 0).
 template <bool CHECK>
 __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __restrict__ act, int n_active, int rows,
-                                                           const float* __restrict__ A1T, int ldt,
+                                                           const float* __restrict__ A1q, int ldq,
                                                            const float* __restrict__ D1, int ldd1,
                                                            const float* __restrict__ D2, int ldd2, float* W0,
                                                            float* V0, int ldw0, int n0, int H, float* W1, float* V1,
@@ -357,7 +325,8 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     const int q4 = ldd2 >> 2;                        // float4 per D2 row (ldd2 % 4 == 0)
     const int lo4 = o4 == 8 ? 3 : 4;                 // log2(o4)
     f32x4* d2s = stage;                              // [ch][o4], columns past ldd2 zero
-    float* a1s = reinterpret_cast<float*>(stage + ch * o4);   // [ch][4]
+    f32x4* a1s = stage + ch * o4;                    // [ch]: activations of rows j0 .. j0+3
+    const f32x4* a1g = reinterpret_cast<const f32x4*>(A1q) + (size_t)min(b, (H - 1) >> 2) * ldq;
     const f32x4* d2g = reinterpret_cast<const f32x4*>(D2);
     const int sub = tid & (o4 - 1), grp = tid >> lo4, ng = 512 >> lo4;
     float acc[16];
@@ -365,35 +334,27 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
     for (int pc = 0; pc < rows; pc += ch) {
       const int cn = min(ch, rows - pc);
-      // one round: ch * o4 = 4096 float4 of D2 (4 per thread) and 4 cn <= 2048
-      // activations (2 per thread), clamped addresses, values selected
+      // one round: ch * o4 = 4096 float4 of D2 (4 per thread) and cn <= 1024
+      // float4 of activations (1 per thread), clamped addresses, values
+      // selected (row H is the bias row: activation 1; rows past it 0)
       {
-        const int nd = cn * o4, na = 4 * cn;
+        const int nd = cn * o4;
         f32x4 v[4];
-        float av[2];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int i = min(tid + u * kTU, nd - 1);
           const int p = i >> lo4, k = i & (o4 - 1);
           v[u] = d2g[(size_t)(pc + p) * q4 + min(k, q4 - 1)];
         }
+        f32x4 av = a1g[pc + min(tid, cn - 1)];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int i = min(tid + u * kTU, na - 1);
-          const int p = i >> 2, j = j0 + (i & 3);
-          const float a = A1T[(size_t)min(j, H - 1) * ldt + pc + p];
-          av[u] = j < H ? a : (j == H ? 1.0f : 0.f);
-        }
+        for (int r = 0; r < 4; ++r) av[r] = j0 + r < H ? av[r] : (j0 + r == H ? 1.0f : 0.f);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int i = tid + u * kTU;
           if (i < nd) d2s[i] = (i & (o4 - 1)) < q4 ? v[u] : f32x4{0.f, 0.f, 0.f, 0.f};
         }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int i = tid + u * kTU;
-          if (i < na) a1s[i] = av[u];
-        }
+        if (tid < cn) a1s[tid] = av;
       }
       __syncthreads();
       if (tid < 512) {
@@ -402,7 +363,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int pp = min(p + u * ng, cn - 1);
-            a[u] = reinterpret_cast<const f32x4*>(a1s)[pp];
+            a[u] = a1s[pp];
             d[u] = d2s[pp * o4 + sub];
           }
 #pragma unroll
@@ -557,35 +518,52 @@ int small_fwdbwd_blocks(int rows) {
   return (rows + P - 1) / P;
 }
 
-size_t small_scratch_floats(int rows, int H) { return rows > 0 ? (size_t)H * rows : 0; }
+size_t small_scratch_floats(int rows, int H) { return rows > 0 ? (size_t)((H + 3) / 4) * 4 * rows : 0; }
+
+template <int P, bool TAB>
+hipError_t launch_fwdbwd_p(hipStream_t s, int nb, size_t lds, const int32_t* act, int n_active, int rows,
+                           const float* W0, int ldw0, int n0, int H, const float* W1, int ldw1, int O, const float* T,
+                           float* A1q, float* D1, int ldd1, float* D2, int ldd2, double* sse_part, const float* tab) {
+  const int hp = small_hp(H), op = small_op(O);
+#define BP_FB(HPV, OPV)                                                                                      \
+  if (hp == HPV && op == OPV)                                                                                \
+    return launch_kernel(small_fwdbwd_kernel<P, TAB, HPV, OPV>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, \
+                         n0, H, W1, ldw1, O, T, A1q, rows, D1, ldd1, D2, ldd2, sse_part, tab);
+  BP_FB(128, 32)
+  BP_FB(128, 64)
+  BP_FB(256, 32)
+  BP_FB(256, 64)
+#undef BP_FB
+  return hipErrorInvalidValue;
+}
 
 template <bool TAB>
 hipError_t launch_fwdbwd(hipStream_t s, int P, int nb, size_t lds, const int32_t* act, int n_active, int rows,
                          const float* W0, int ldw0, int n0, int H, const float* W1, int ldw1, int O, const float* T,
-                         float* A1T, float* D1, int ldd1, float* D2, int ldd2, double* sse_part, const float* tab) {
+                         float* A1q, float* D1, int ldd1, float* D2, int ldd2, double* sse_part, const float* tab) {
   switch (P) {
-    case 1: return launch_kernel(small_fwdbwd_kernel<1, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
-    case 2: return launch_kernel(small_fwdbwd_kernel<2, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
-    case 4: return launch_kernel(small_fwdbwd_kernel<4, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
-    default: return launch_kernel(small_fwdbwd_kernel<8, TAB>, nb, kT, lds, s, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, rows, D1, ldd1, D2, ldd2, sse_part, tab);
+    case 1: return launch_fwdbwd_p<1, TAB>(s, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1, D2, ldd2, sse_part, tab);
+    case 2: return launch_fwdbwd_p<2, TAB>(s, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1, D2, ldd2, sse_part, tab);
+    case 4: return launch_fwdbwd_p<4, TAB>(s, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1, D2, ldd2, sse_part, tab);
+    default: return launch_fwdbwd_p<8, TAB>(s, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1, D2, ldd2, sse_part, tab);
   }
 }
 
 hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int rows, const float* W0, int ldw0, int n0,
-                        int H, const float* W1, int ldw1, int O, const float* T, float* A1T, float* D1, int ldd1,
+                        int H, const float* W1, int ldw1, int O, const float* T, float* A1q, float* D1, int ldd1,
                         float* D2, int ldd2, double* sse_part, const float* tab) {
   if (rows <= 0) return hipSuccess;
   const int P = patterns_per_block(rows);
   const size_t lds = sizeof(float) * small_fwdbwd_lds_floats(P, H, O, n_active);
   const int nb = small_fwdbwd_blocks(rows);
   if (tab)
-    return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, D1, ldd1,
+    return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1,
                                D2, ldd2, sse_part, tab);
-  return launch_fwdbwd<false>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1T, D1, ldd1, D2,
+  return launch_fwdbwd<false>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1, D2,
                               ldd2, sse_part, tab);
 }
 
-hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1T, const float* D1,
+hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1q, const float* D1,
                         int ldd1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
                         float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults) {
   if (rows <= 0) return hipSuccess;
@@ -595,9 +573,9 @@ hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int row
   // tile chunks: ch (o4 + 1) float4; bias-row chunks: 512 rows of 8 float4
   const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1), (size_t)512 * 8);
   if (limit > 0.f)
-    return launch_kernel(small_update_kernel<true>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1T, rows, D1,
+    return launch_kernel(small_update_kernel<true>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1q, rows, D1,
                          ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
-  return launch_kernel(small_update_kernel<false>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1T, rows, D1,
+  return launch_kernel(small_update_kernel<false>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1q, rows, D1,
                        ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
 }
 
