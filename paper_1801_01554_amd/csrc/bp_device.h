@@ -44,6 +44,15 @@ __device__ __forceinline__ float checked_change(float g, float limit, int& fault
   return g;
 }
 
+// The momentum step V = lr G + mom V (section 6.2.1) with its rounding
+// fixed: mom V is rounded, lr G is fused into the add.  Written out so that
+// no kernel or template instance is left to the compiler's choice of which
+// product to fuse, which would change the last bit between otherwise equal
+// code paths.
+__device__ __forceinline__ float momentum_step(float g, float v_old, float lr, float mom) {
+  return fmaf(lr, g, mom * v_old);
+}
+
 // Adds the fault counts of a wave to the device counter: a wave sum, then one
 // atomic from lane 0 when the sum is nonzero.  Every lane of the wave must
 // reach this call.

@@ -131,7 +131,7 @@ struct EpiUpdate {
     int f = 0;
     const float g = checked_change(acc, limit, f);
     nf += (float)f;
-    const float v = lr * g + mom * vw.x;
+    const float v = momentum_step(g, vw.x, lr, mom);
     V[i] = v;
     W[i] = vw.y + v;
     return 0.f;
@@ -492,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __
     for (int z = 0; z < splits; ++z) g += P[z * split_stride + (size_t)m * ldp + n];
     g = checked_change(g, limit, nf);
     const size_t i = (size_t)m * ldw + n;
-    const float v = lr * g + mom * V[i];
+    const float v = momentum_step(g, V[i], lr, mom);
     V[i] = v;
     W[i] = W[i] + v;
   }
@@ -602,7 +602,7 @@ __global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(const floa
       float g = 0.f;
       for (int w = 0; w < kBiasWaves; ++w) g += part[w][lane];
       g = checked_change(g, limit, nf);
-      const float v = lr * g + mom * Vb[n];
+      const float v = momentum_step(g, Vb[n], lr, mom);
       Vb[n] = v;
       Wb[n] = Wb[n] + v;
     }
@@ -693,7 +693,7 @@ __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* 
   if (col < H) {
     g = checked_change(g, limit, nf);
     const size_t i = (size_t)r * ldw + col;
-    const float v = lr * g + mom * V[i];
+    const float v = momentum_step(g, V[i], lr, mom);
     V[i] = v;
     W[i] = W[i] + v;
   }

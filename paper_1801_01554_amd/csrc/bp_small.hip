@@ -253,9 +253,12 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
 // Op / 4 float4 plus one float4 of activations each): 4096 float4 of D2.
 __host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 / (small_op(O) / 4); }
 
-// 1024 threads = 16 waves per block.  The weight and momentum a lane updates
-// are loaded at the start, overlapping the sums.  Batch sums run over chunks
-// of `ch` patterns staged in LDS by one round of coalesced loads.
+// 1024 threads = 16 waves per block.  The weight and momentum a thread
+// updates are loaded in the block's first round of loads (loads that are
+// still in flight at a loop head are waited for there, so they cannot be
+// issued ahead of it).  Batch sums run over chunks of `ch` patterns staged in
+// LDS by one round of coalesced loads, every load stored unconditionally so
+// that none is sunk behind a branch.
 // Blocks [0, nT): rows j0 .. j0+3 of W1 (j0 = 4 b; row H is the bias row,
 //   activation 1), all O columns: G[j][c] = sum_p A1[p][j] D2[p][c].  Waves
 //   0-7 compute: lane (sub, g) holds the 4 x 4 tile of rows j0 .. j0+3 and
@@ -264,8 +267,9 @@ __host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 
 //   through LDS in a fixed tree.
 // Blocks [nT, nT + n0): row r of W0: the delta rows of the patterns whose
 //   active list holds r, in pattern order (ballot compaction of 1024
-//   patterns at a time); wave w owns the column strip (w % 4) and quarter
-//   (w / 4) of each compacted list.
+//   patterns at a time); with ns = 1, 2 or 4 strips of 64 columns covering
+//   H, wave w owns the column strip w % ns and the slice w / ns (of 16 / ns
+//   equal slices) of each compacted list.
 // Blocks [nT + n0, nT + n0 + nS): the bias row of W0, 32 columns per block:
 //   sum_p D1[p][j], the half-wave h of wave w adding the (2 w + h)-th of 32
 //   slices of each chunk in pattern order, the 32 slice sums combined in
@@ -300,11 +304,12 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     ncol = j <= H ? O : 0;
     owner = tid < 4 * Op;                            // whole waves
   } else if (b < nT + n0) {
+    const int ns = H <= 64 ? 1 : (H <= 128 ? 2 : 4);
     Wt = W0 + (size_t)(b - nT) * ldw0;
     Vt = V0 + (size_t)(b - nT) * ldw0;
-    col = (wave & 3) * 64 + lane;
+    col = (wave & (ns - 1)) * 64 + lane;
     ncol = H;
-    owner = wave < 4;
+    owner = wave < ns;
   } else {
     Wt = W0 + (size_t)n0 * ldw0;
     Vt = V0 + (size_t)n0 * ldw0;
@@ -313,11 +318,8 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     owner = wave == 0;
   }
   const bool live = col < ncol;
+  const bool upd = owner && live;
   float w_old = 0.f, v_old = 0.f;
-  if (owner && live) {
-    w_old = Wt[col];
-    v_old = Vt[col];
-  }
 
   float g = 0.f;
   if (b < nT) {
@@ -325,7 +327,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     const int q4 = ldd2 >> 2;                        // float4 per D2 row (ldd2 % 4 == 0)
     const int lo4 = o4 == 8 ? 3 : 4;                 // log2(o4)
     f32x4* d2s = stage;                              // [ch][o4], columns past ldd2 zero
-    f32x4* a1s = stage + ch * o4;                    // [ch]: activations of rows j0 .. j0+3
+    f32x4* a1s = stage + ch * o4;                    // [ch + 64]: activations of rows j0 .. j0+3
     const f32x4* a1g = reinterpret_cast<const f32x4*>(A1q) + (size_t)min(b, (H - 1) >> 2) * ldq;
     const f32x4* d2g = reinterpret_cast<const f32x4*>(D2);
     const int sub = tid & (o4 - 1), grp = tid >> lo4, ng = 512 >> lo4;
@@ -339,6 +341,10 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       // selected (row H is the bias row: activation 1; rows past it 0)
       {
         const int nd = cn * o4;
+        if (pc == 0 && upd) {
+          w_old = Wt[col];
+          v_old = Vt[col];
+        }
         f32x4 v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -350,11 +356,11 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
 #pragma unroll
         for (int r = 0; r < 4; ++r) av[r] = j0 + r < H ? av[r] : (j0 + r == H ? 1.0f : 0.f);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < 4; ++u) {             // ch * o4 = 4 kTU slots
           const int i = tid + u * kTU;
-          if (i < nd) d2s[i] = (i & (o4 - 1)) < q4 ? v[u] : f32x4{0.f, 0.f, 0.f, 0.f};
+          d2s[i] = (i < nd && (i & (o4 - 1)) < q4) ? v[u] : f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        if (tid < cn) a1s[tid] = av;
+        a1s[tid < ch ? tid : ch + lane] = av;
       }
       __syncthreads();
       if (tid < 512) {
@@ -406,9 +412,13 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     if (owner) g = tile_sum[tid];                       // tid = jj Op + col
   } else if (b < nT + n0) {
     const int r = b - nT;
-    const int quarter = wave >> 2;
+    const int ns = H <= 64 ? 1 : (H <= 128 ? 2 : 4), nsl = kWU / ns, slice = wave / ns;
     for (int pc = 0; pc < rows; pc += kTU) {
       const int p = pc + tid;
+      if (pc == 0 && upd) {
+        w_old = Wt[col];
+        v_old = Vt[col];
+      }
       bool hit = false;
       if (p < rows) {
         const int32_t* a = act + (size_t)p * n_active;
@@ -432,22 +442,23 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       }
       if (hit) list[base + __popcll(bal & ((1ull << lane) - 1ull))] = p;
       __syncthreads();
-      const int q0 = (int)((int64_t)total * quarter / 4), q1 = (int)((int64_t)total * (quarter + 1) / 4);
+      const int q0 = (int)((int64_t)total * slice / nsl), q1 = (int)((int64_t)total * (slice + 1) / nsl);
       float s = 0.f;
       if (live) {
-        for (int q = q0; q < q1; q += 16) {
-          float v[16];
+        for (int q = q0; q < q1; q += 4) {
+          float v[4];
 #pragma unroll
-          for (int u = 0; u < 16; ++u) v[u] = D1[(size_t)list[min(q + u, q1 - 1)] * ldd1 + col];
+          for (int u = 0; u < 4; ++u) v[u] = D1[(size_t)list[min(q + u, q1 - 1)] * ldd1 + col];
 #pragma unroll
-          for (int u = 0; u < 16; ++u)
+          for (int u = 0; u < 4; ++u)
             if (q + u < q1) s += v[u];
         }
       }
-      // quarters of this chunk are added to the running sum in list order
+      // the slices of this chunk are added to the running sum in list order
       part[wave][lane] = s;
       __syncthreads();
-      if (owner) g = (((g + part[wave][lane]) + part[wave + 4][lane]) + part[wave + 8][lane]) + part[wave + 12][lane];
+      if (owner)
+        for (int k = 0; k < nsl; ++k) g += part[k * ns + wave][lane];
       __syncthreads();
     }
   } else {
@@ -458,6 +469,10 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     f32x4* d1s = stage;                              // [512][8]
     for (int pc = 0; pc < rows; pc += 512) {
       const int cn = min(512, rows - pc), nd = cn * 8;
+      if (pc == 0 && upd) {
+        w_old = Wt[col];
+        v_old = Vt[col];
+      }
       f32x4 v[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -466,8 +481,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         v[u] = *reinterpret_cast<const f32x4*>(D1 + (size_t)(pc + (i >> 3)) * ldd1 + cc);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (tid + u * kTU < nd) d1s[tid + u * kTU] = v[u];
+      for (int u = 0; u < 4; ++u) d1s[tid + u * kTU] = v[u];   // 512 x 8 slots; past nd unread
       __syncthreads();
       const int sl = 2 * wave + h, s0 = cn * sl / 32, s1 = cn * (sl + 1) / 32;
       const float* col_s = reinterpret_cast<const float*>(d1s) + c;
@@ -489,9 +503,9 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
   }
   if (owner) {   // whole waves
     int nf = 0;
-    if (live) {
+    if (upd) {
       if (CHECK) g = checked_change(g, limit, nf);
-      const float v = lr * g + mom * v_old;
+      const float v = momentum_step(g, v_old, lr, mom);
       Vt[col] = v;
       Wt[col] = w_old + v;
     }
@@ -570,8 +584,8 @@ hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int row
   const int nT = (H + 1 + 3) / 4;
   const int nS = (H + 31) / 32;
   const int ch = small_update_chunk(O), o4 = small_op(O) / 4;
-  // tile chunks: ch (o4 + 1) float4; bias-row chunks: 512 rows of 8 float4
-  const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1), (size_t)512 * 8);
+  // tile chunks: ch (o4 + 1) + 64 float4; bias-row chunks: 512 rows of 8 float4
+  const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1) + 64, (size_t)512 * 8);
   if (limit > 0.f)
     return launch_kernel(small_update_kernel<true>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1q, rows, D1,
                          ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
