@@ -231,6 +231,18 @@ enum {
   BP_K_COUNT = 13
 };
 
+/* Graph replay of repeated training calls (on by default).  With on != 0,
+ * a call of bp_train_batches / bp_train_batches_onehot whose arguments (data
+ * pointers, sizes, lr, momentum) equal those of the previous call captures
+ * its kernel launches into a HIP graph, and later calls with the same
+ * arguments replay that graph instead of launching each kernel: same
+ * kernels, same results bit for bit, less launch overhead per update.  A
+ * change of workspace size, sigmoid mode or range check, or profiling,
+ * drops back to direct launches.  The graph reads the argument buffers at
+ * replay time, so their contents may change between calls.  on == 0: every
+ * call launches directly.  Waits for the net's stream; drops any graph. */
+int bp_set_graph_replay(bp_net* net, int on);
+
 /* on != 0: from now on every kernel launch of this net is bracketed by HIP
  * events on the net's stream (adds launch overhead; for measurement runs
  * only); clears the counters.  on == 0: stops recording. */

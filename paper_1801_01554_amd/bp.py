@@ -25,7 +25,7 @@ BP_OK, BP_EINVAL, BP_ENOMEM, BP_EDEVICE = 0, -1, -2, -3
 EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set_weights", "bp_get_weights",
            "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
            "bp_forward_onehot", "bp_set_context", "bp_train_sequences", "bp_forward_sequences", "bp_set_sigmoid", "bp_set_fault_limit", "bp_get_fault_count",
-           "bp_checkpoint_save", "bp_checkpoint_restore", "bp_guard_config", "bp_guard_epoch", "bp_profile",
+           "bp_checkpoint_save", "bp_checkpoint_restore", "bp_guard_config", "bp_guard_epoch", "bp_set_graph_replay", "bp_profile",
            "bp_profile_report", "bp_last_error")
 BP_SIGMOID_EXACT, BP_SIGMOID_TABLE = 0, 1
 KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce", "fused_fb",
@@ -78,6 +78,7 @@ def lib():
         "bp_checkpoint_restore": (ctypes.c_int, [_vp]),
         "bp_guard_config": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double]),
         "bp_guard_epoch": (ctypes.c_int, [_vp, ctypes.c_double, ctypes.POINTER(ctypes.c_int32)]),
+        "bp_set_graph_replay": (ctypes.c_int, [_vp, ctypes.c_int]),
         "bp_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
         "bp_profile_report": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64), _f64p, ctypes.c_int32]),
         "bp_last_error": (ctypes.c_char_p, [_vp]),
@@ -199,6 +200,10 @@ def bp_guard_epoch(h, sse: float):
     r = ctypes.c_int32(0)
     rc = lib().bp_guard_epoch(h, float(sse), ctypes.byref(r))
     return rc, int(r.value)
+
+
+def bp_set_graph_replay(h, on: bool) -> int:
+    return lib().bp_set_graph_replay(h, 1 if on else 0)
 
 
 def bp_profile(h, on: bool) -> int:
@@ -343,6 +348,10 @@ class Net:
         rc, r = bp_guard_epoch(self._h, sse)
         self._chk(rc)
         return r
+
+    def set_graph_replay(self, on: bool) -> None:
+        """Replay repeated training calls from a captured HIP graph (default on)."""
+        self._chk(bp_set_graph_replay(self._h, on))
 
     def profile(self, on: bool) -> None:
         self._chk(bp_profile(self._h, on))

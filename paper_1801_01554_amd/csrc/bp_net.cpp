@@ -82,6 +82,30 @@ struct bp_net {
   std::vector<hipEvent_t> ev_pool;
   int64_t prof_n[BP_K_COUNT] = {};
   double prof_ms[BP_K_COUNT] = {};
+  // graph replay of a repeated training call: the second of two calls with
+  // the same arguments captures its launches into a HIP graph, and later
+  // calls with those arguments replay it.  `gen` changes whenever something
+  // a captured call depends on changes (workspace, sigmoid, range check).
+  struct TrainKey {
+    const void* x = nullptr;
+    const void* act = nullptr;
+    const void* t = nullptr;
+    int64_t n = 0;
+    int32_t batch = 0, n_active = 0, ldx = 0;
+    uint32_t lr = 0, mom = 0;
+    uint64_t gen = 0;
+    bool operator==(const TrainKey& o) const {
+      return x == o.x && act == o.act && t == o.t && n == o.n && batch == o.batch && n_active == o.n_active &&
+             ldx == o.ldx && lr == o.lr && mom == o.mom && gen == o.gen;
+    }
+  };
+  bool graph_on = true;
+  uint64_t gen = 0;
+  bool have_last = false;
+  TrainKey last_key, graph_key;
+  hipStream_t cap_stream = nullptr;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
   std::string err;
 };
 
@@ -161,6 +185,7 @@ void free_workspace(bp_net* net) {
   free_ptr(net->splitk);
   net->splitk = nullptr;
   net->splitk_cap = 0;
+  ++net->gen;
 }
 
 // Floats of split-K workspace one forward pass over `fwd_rows` patterns and
@@ -208,6 +233,7 @@ int ensure_sse(bp_net* net, size_t count) {
   net->sse_cap = 0;
   BP_HIP(net, hipMalloc(&net->sse_part, sizeof(double) * count));
   net->sse_cap = count;
+  ++net->gen;
   return BP_OK;
 }
 
@@ -350,26 +376,12 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
   return BP_OK;
 }
 
-int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr, float mom,
-          double* sse_out) {
-  if (n == 0) {
-    if (sse_out) *sse_out = 0.0;
-    return BP_OK;
-  }
-  const int64_t rows_max = std::min<int64_t>(batch, n);
-  // every batch but the last has rows_max rows
-  const int64_t nb = (n + batch - 1) / batch;
-  const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
-  size_t sk = std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows));
-  if (use_small(net, in))   // the fused path's transposed activations take the split-K workspace
-    sk = std::max(sk, bpk::small_scratch_floats((int)rows_max, net->n[1]));
-  int rc = ensure_workspace(net, rows_max, 0, sk);
-  if (rc) return rc;
-  // exact number of error partials
-  const size_t need = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +
-                      (size_t)sse_blocks(net, in, last_rows);
-  rc = ensure_sse(net, need);
-  if (rc) return rc;
+// The launches of one training call: every batch, then the error reduction
+// (kernels only, on net->stream; no allocation, copy or synchronisation, so
+// that the sequence can be captured into a graph).
+int train_launches(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr,
+                   float mom) {
+  int rc = BP_OK;
   size_t used = 0;
   for (int64_t p0 = 0; p0 < n; p0 += batch) {
     const int rows = (int)std::min<int64_t>(batch, n - p0);
@@ -390,6 +402,95 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
     if (rc) return rc;
   }
   BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(net->stream, net->sse_part, (int)used, net->sse_dev));
+  return BP_OK;
+}
+
+void drop_graph(bp_net* net) {
+  if (net->graph_exec) (void)hipGraphExecDestroy(net->graph_exec);
+  if (net->graph) (void)hipGraphDestroy(net->graph);
+  net->graph_exec = nullptr;
+  net->graph = nullptr;
+}
+
+// Captures train_launches on the net's private capture stream and
+// instantiates the graph (replacing the previous one).
+int capture_train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr,
+                  float mom) {
+  if (!net->cap_stream) BP_HIP(net, hipStreamCreateWithFlags(&net->cap_stream, hipStreamNonBlocking));
+  drop_graph(net);
+  BP_HIP(net, hipStreamBeginCapture(net->cap_stream, hipStreamCaptureModeThreadLocal));
+  hipStream_t user = net->stream;
+  net->stream = net->cap_stream;
+  const int rc = train_launches(net, in, targets, n, batch, lr, mom);
+  net->stream = user;
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(net->cap_stream, &g);
+  if (rc) {
+    if (g) (void)hipGraphDestroy(g);
+    return rc;
+  }
+  if (e != hipSuccess) return hip_fail(net, e, "hipStreamEndCapture");
+  hipGraphExec_t ex = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+  if (ei != hipSuccess) {
+    (void)hipGraphDestroy(g);
+    return hip_fail(net, ei, "hipGraphInstantiate");
+  }
+  net->graph = g;
+  net->graph_exec = ex;
+  return BP_OK;
+}
+
+int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr, float mom,
+          double* sse_out) {
+  if (n == 0) {
+    if (sse_out) *sse_out = 0.0;
+    return BP_OK;
+  }
+  const int64_t rows_max = std::min<int64_t>(batch, n);
+  // every batch but the last has rows_max rows
+  const int64_t nb = (n + batch - 1) / batch;
+  const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
+  size_t sk = std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows));
+  if (use_small(net, in))   // the fused path's grouped activations take the split-K workspace
+    sk = std::max(sk, bpk::small_scratch_floats((int)rows_max, net->n[1]));
+  int rc = ensure_workspace(net, rows_max, 0, sk);
+  if (rc) return rc;
+  // exact number of error partials
+  const size_t need = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +
+                      (size_t)sse_blocks(net, in, last_rows);
+  rc = ensure_sse(net, need);
+  if (rc) return rc;
+  if (net->graph_on && !net->prof) {
+    bp_net::TrainKey key;
+    key.x = in.x;
+    key.act = in.act;
+    key.t = targets;
+    key.n = n;
+    key.batch = batch;
+    key.n_active = in.n_active;
+    key.ldx = in.ldx;
+    std::memcpy(&key.lr, &lr, sizeof(float));
+    std::memcpy(&key.mom, &mom, sizeof(float));
+    key.gen = net->gen;
+    if (!(net->graph_exec && key == net->graph_key)) {
+      if (net->have_last && key == net->last_key) {
+        rc = capture_train(net, in, targets, n, batch, lr, mom);
+        if (rc) return rc;
+        net->graph_key = key;
+      } else {
+        rc = train_launches(net, in, targets, n, batch, lr, mom);
+        if (rc) return rc;
+        net->last_key = key;
+        net->have_last = true;
+        key.n = -1;   // no replay this time
+      }
+    }
+    if (key.n >= 0) BP_HIP(net, hipGraphLaunch(net->graph_exec, net->stream));
+  } else {
+    rc = train_launches(net, in, targets, n, batch, lr, mom);
+    if (rc) return rc;
+  }
   if (sse_out) {
     BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, net->stream));
     BP_HIP(net, hipStreamSynchronize(net->stream));
@@ -638,6 +739,8 @@ void bp_destroy(bp_net* net) {
     (void)hipEventDestroy(r.b);
   }
   for (hipEvent_t e : net->ev_pool) (void)hipEventDestroy(e);
+  drop_graph(net);
+  if (net->cap_stream) (void)hipStreamDestroy(net->cap_stream);
   delete net;
 }
 
@@ -739,6 +842,15 @@ int bp_forward_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, 
   in.act = active_dev;
   in.n_active = n_active;
   return forward_only(net, in, n_patterns, outputs_dev);
+}
+
+int bp_set_graph_replay(bp_net* net, int on) {
+  if (check_net(net)) return BP_EINVAL;
+  BP_HIP(net, hipStreamSynchronize(net->stream));
+  net->graph_on = on != 0;
+  net->have_last = false;
+  drop_graph(net);
+  return BP_OK;
 }
 
 int bp_profile(bp_net* net, int on) {
@@ -846,6 +958,7 @@ int bp_set_sigmoid(bp_net* net, int32_t mode) {
   BP_HIP(net, hipStreamSynchronize(net->stream));
   if (mode == BP_SIGMOID_EXACT) {
     net->sig_tab = nullptr;
+    ++net->gen;
     return BP_OK;
   }
   if (!net->sig_tab_mem) {
@@ -859,6 +972,7 @@ int bp_set_sigmoid(bp_net* net, int32_t mode) {
     BP_HIP(net, hipMemcpy(net->sig_tab_mem, host, sizeof(host), hipMemcpyHostToDevice));
   }
   net->sig_tab = net->sig_tab_mem;
+  ++net->gen;
   return BP_OK;
 }
 
@@ -870,6 +984,7 @@ int bp_set_fault_limit(bp_net* net, float limit) {
   const unsigned long long zero = 0;
   BP_HIP(net, hipMemcpy(net->faults, &zero, sizeof(zero), hipMemcpyHostToDevice));
   net->fault_limit = limit;
+  ++net->gen;
   return BP_OK;
 }
 

@@ -67,4 +67,5 @@ def test_null_net_is_rejected(bp):
     assert L.bp_guard_config(None, 1, 2.0) == bp.BP_EINVAL
     assert L.bp_guard_epoch(None, 1.0, None) == bp.BP_EINVAL
     assert L.bp_profile(None, 1) == bp.BP_EINVAL
+    assert L.bp_set_graph_replay(None, 1) == bp.BP_EINVAL
     L.bp_destroy(None)   # no-op
