@@ -131,6 +131,29 @@ def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     _check_update(w, dev, batch, 0.05, 0.9, what="ragged")
 
 
+# --------------------------------------------------------------------------- fused path instances
+# The fused small-net kernels are compiled per patterns-per-block P (1, 2, 4
+# or 8, from the batch: 1 below 512 rows, 2 from 512, 4 from 1024, 8 from
+# 2048) and per padded layer sizes (hidden units to 128 or 256, outputs to
+# 32 or 64).  Each case runs a full batch and a ragged 37-row batch (P = 1,
+# a partly filled last block) through every pair of padded sizes.
+@pytest.mark.parametrize("hidden,outs", [(100, 20), (100, 50), (200, 20), (200, 50)])
+@pytest.mark.parametrize("batch", [100, 600, 1100, 2100])
+def test_fused_path_instances(dev, hidden, outs, batch):
+    w = wl.make_custom((203, hidden, outs), batch + 37, seed=hidden + outs + batch, onehot=True,
+                       init="uniform0.3")
+    _check_update(w, dev, batch, 0.05, 0.9, what="fused instance")
+
+
+@pytest.mark.parametrize("n_active", [1, 12, 32])
+def test_fused_path_active_counts(dev, n_active):
+    """Patterns with 1, 12 and 32 active inputs (the gather's unrolled part and its tail)."""
+    w = wl.make_custom((203, 120, 26), 700, seed=40 + n_active, onehot=True, init="uniform0.3")
+    g = np.random.default_rng(n_active)
+    w.active = np.stack([g.permutation(203)[:n_active] for _ in range(700)]).astype(np.int32)
+    _check_update(w, dev, 512, 0.05, 0.9, what=f"fused path, {n_active} active inputs")
+
+
 # --------------------------------------------------------------------------- epochs
 @pytest.mark.parametrize("name", ["nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16"])
 def test_epoch_errors_nettalk(dev, name):
