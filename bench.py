@@ -90,7 +90,7 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
             add("gather", R * no * (n_active + 1), 4 * (R * n_active + (ni + 1) * no + R * no))
             add("scatter", R * no * (n_active + 1), 4 * (R * n_active + R * no) + 16 * (ni + 1) * no)
         else:
-            if fwd and l == L - 1 and splits_of(rows, no, ni) > 1:
+            if fwd and l == L - 1 and choose_output_splits(rows, no, ni) > 1:
                 add("output", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no))
                 add("output_finish", 6 * R * no, 4 * (2 * R * no + no))
             elif fwd and l == L - 1:
@@ -123,6 +123,14 @@ def seq_kind_work(sizes, n_ctx, S, steps, splits_of):
         f0, b0 = w.get(k, (0.0, 0.0))
         w[k] = (f0 + f, b0 + b)
     return w
+
+
+def choose_output_splits(M, N, K):
+    """Mirror of the library's split-K choice for the output layer (products with few tiles and
+    K <= 2048 take the skinny kernel, unsplit), for work accounting only."""
+    if K <= 2048 and -(-M // 64) * -(-N // 64) < 128:
+        return 1
+    return choose_splits(M, N, K)
 
 
 def choose_splits(M, N, K):
@@ -347,6 +355,9 @@ def kind_of_kernel(name):
             return "change" if m.group(1) == "true" else "output"
         return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
                 "EpiUpdate": "change"}.get(epi)
+    m = re.search(r"skinny_kernel<\d+, (true|false), (true|false), (true|false), [^>]*?(\w+)>", name)
+    if m:
+        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward"}.get(m.group(4))
     for k, v in KERNEL_NAMES.items():
         if "<" not in v and v in name:
             return k

@@ -478,6 +478,181 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 }
 
 // --------------------------------------------------------------------------
+// Products with few output tiles (an Elman net's per-step layers: M = the
+// sequence streams, N = the layer, K = the layer below).  A 64 x 64 tile grid
+// would keep a fraction of the CUs busy, each wave with a long chain of
+// dependent loads and MFMAs.  Here a block owns RB 32 x 32 MFMA blocks of
+// one 32-column strip (a 32 RB-row tile) and splits K over four wave groups:
+// wave w works on row block w % RB and K group w / RB.  K is cut into four
+// ranges of KC = 2 KH values, KH a multiple of 16; within a range, MFMA step
+// i pairs k = k0 + i (lanes 0-31) with k = k0 + KH + i (lanes 32-63), so that
+// each lane reads its A row (and its B row when B is stored [n][k])
+// contiguously.  Each lane loads its operands straight from global memory,
+// 16 steps at a time with the next 32 in flight.  The four K partials of a
+// row block are added through LDS in K order, and the four waves of the row
+// block share its epilogue (RB = 2 for epilogues with 64-row column sums).
+constexpr int kSkinnyChunk = 16;   // MFMA steps per load round
+
+inline bool use_skinny(int M, int N, int K) { return K <= 2048 && tiles_of(M, N, 64) < 128; }
+
+template <int RB, bool B_NK, bool AVEC, bool BVEC, class Epi>
+__global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restrict__ A, int lda,
+                                                          const float* __restrict__ B, int ldb, int M, int N,
+                                                          int K, Epi epi) {
+  static_assert(!Epi::kFaults, "update epilogues take gemm_kernel");
+  static_assert(!Epi::kColSum || RB == 2, "64-row column sums need RB = 2");
+  constexpr int C = kSkinnyChunk;
+  __shared__ float part[4][RB][16][64];
+  const int tiles_n = (N + 31) / 32;
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+  const int m0 = tm * 32 * RB, n0 = tn * 32;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rb = wave % RB, kg = wave / RB;
+  const int r = lane & 31, h = lane >> 5;
+  const int kh = ((K + 7) / 8 + C - 1) / C * C;      // KH
+  const int kbase = kg * 2 * kh + h * kh;            // this lane's first k
+  const int m = m0 + rb * 32 + r, n = n0 + r;        // A row and B column of this lane
+  const int mc = min(m, M - 1), nc = min(n, N - 1);
+  const float* arow = A + (size_t)mc * lda;
+
+  // operands of MFMA steps c C .. c C + C - 1 (zero past K, M or N).  Every
+  // load reads a clamped, valid address and is issued before any mask is
+  // applied; masks are bitwise ANDs, so the compiler has no branch to sink a
+  // load into (a load sunk behind a predicate waits for itself) and masked
+  // elements are exact zeros.
+  const int mrow = m < M ? -1 : 0, ncol = n < N ? -1 : 0;
+  auto masked = [](float v, int keep) { return __builtin_bit_cast(float, __builtin_bit_cast(int, v) & keep); };
+  auto load = [&](int c, float* a, float* b) {
+    const int k0 = kbase + c * C;
+    if (AVEC) {
+      f32x4 v[C / 4];
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q) v[q] = *reinterpret_cast<const f32x4*>(arow + min(k0 + 4 * q, lda - 4));
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < K ? mrow : 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i) a[i] = arow[min(k0 + i, K - 1)];
+#pragma unroll
+      for (int i = 0; i < C; ++i) a[i] = masked(a[i], k0 + i < K ? mrow : 0);
+    }
+    if (B_NK && BVEC) {
+      const float* brow = B + (size_t)nc * ldb;
+      f32x4 v[C / 4];
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q) v[q] = *reinterpret_cast<const f32x4*>(brow + min(k0 + 4 * q, ldb - 4));
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) b[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < K ? ncol : 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        b[i] = B_NK ? B[(size_t)nc * ldb + min(k0 + i, K - 1)] : B[(size_t)min(k0 + i, K - 1) * ldb + nc];
+#pragma unroll
+      for (int i = 0; i < C; ++i) b[i] = masked(b[i], k0 + i < K ? ncol : 0);
+    }
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  // three register sets: chunks c + 1 and c + 2 are in flight while chunk c
+  // is multiplied (up to three chunks, K <= 384, all loads precede the first
+  // MFMA)
+  const int nchunk = kh / C;
+  float a0[C], b0[C], a1[C], b1[C], a2[C], b2[C];
+  auto mfma = [&](const float* a, const float* b) {
+#pragma unroll
+    for (int i = 0; i < C; ++i) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[i], acc, 0, 0, 0);
+  };
+  if (nchunk > 0) load(0, a0, b0);
+  if (nchunk > 1) load(1, a1, b1);
+  for (int c = 0; c < nchunk; c += 3) {
+    if (c + 2 < nchunk) load(c + 2, a2, b2);
+    mfma(a0, b0);
+    if (c + 1 >= nchunk) break;
+    if (c + 3 < nchunk) load(c + 3, a0, b0);
+    mfma(a1, b1);
+    if (c + 2 >= nchunk) break;
+    if (c + 4 < nchunk) load(c + 4, a1, b1);
+    mfma(a2, b2);
+  }
+
+  // The K partials go through LDS; wave (rb, kg) then adds, in K-group
+  // order, registers 4 kg .. 4 kg + 3 of its row block (rows 8 kg + 4 h + q
+  // of the 32 x 32 block: register e of lane (h, r) holds row 8 (e / 4) +
+  // 4 h + (e % 4), column r) and applies the epilogue to them, so that all
+  // waves share the epilogue.
+#pragma unroll
+  for (int e = 0; e < 16; ++e) part[kg][rb][e][lane] = acc[e];
+  __syncthreads();
+  float sse = 0.f, csum = 0.f;
+  if (n < N) {
+    const float cv = epi.column(n);
+    float v[4];
+    typename Epi::Pre pre[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * kg + q;
+      v[q] = ((part[0][rb][e][lane] + part[1][rb][e][lane]) + part[2][rb][e][lane]) + part[3][rb][e][lane];
+      pre[q] = epi.load(min(m0 + rb * 32 + 8 * kg + 4 * h + q, M - 1), n);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int mm = m0 + rb * 32 + 8 * kg + 4 * h + q;
+      if (mm < M) csum += epi.apply(mm, n, v[q], cv, pre[q], sse);
+    }
+  }
+  if constexpr (Epi::kColSum) {
+    // the 64-row tile's column sums: per wave over its 8 rows (lanes h = 0,
+    // 1 hold the same column), then the waves in (row block, K group) order
+    __shared__ float cs[2][4][32];
+    const float v = csum + __shfl_xor(csum, 32, 64);
+    if (h == 0) cs[rb][kg][r] = v;
+    __syncthreads();
+    if (threadIdx.x < 32 && n0 + (int)threadIdx.x < N) {
+      float t = 0.f;
+#pragma unroll
+      for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) t += cs[b2][g][threadIdx.x];
+      epi.colsum[(size_t)tm * epi.ldcs + n0 + threadIdx.x] = t;
+    }
+  }
+  if constexpr (Epi::kSSE) {
+    __shared__ float red[4 * RB];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+    if (lane == 0) red[wave] = sse;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double s = 0.0;
+      for (int w = 0; w < 4 * RB; ++w) s += (double)red[w];
+      epi.sse_part[blockIdx.x] = s;
+    }
+  }
+}
+
+template <int RB, bool B_NK, class Epi>
+hipError_t launch_skinny(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
+                         const Epi& epi) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const int tiles = ((M + 32 * RB - 1) / (32 * RB)) * ((N + 31) / 32);
+  const bool avec = (lda % 4 == 0) && ((reinterpret_cast<uintptr_t>(A) & 15) == 0);
+  const bool bvec = B_NK && (ldb % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) & 15) == 0);
+  if (avec && bvec)
+    return launch_kernel(skinny_kernel<RB, B_NK, true, true, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+  if (avec)
+    return launch_kernel(skinny_kernel<RB, B_NK, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+  if (bvec)
+    return launch_kernel(skinny_kernel<RB, B_NK, false, true, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+  return launch_kernel(skinny_kernel<RB, B_NK, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+}
+
+// --------------------------------------------------------------------------
 // Split-K reduction of the change followed by the momentum update.
 __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __restrict__ P, int splits,
                                                                  size_t split_stride, int M, int N, int ldp,
@@ -733,7 +908,7 @@ int choose_splits(int M, int N, int K) {
   return s < 1 ? 1 : s;
 }
 
-int choose_output_splits(int M, int N, int K) { return choose_splits(M, N, K); }
+int choose_output_splits(int M, int N, int K) { return use_skinny(M, N, K) ? 1 : choose_splits(M, N, K); }
 
 int chunk_for(int K, int splits) {
   int c = (K + splits - 1) / splits;
@@ -753,6 +928,7 @@ LaunchEvents& launch_events() {
 int colsum_rows(int M) { return (M + 63) / 64; }
 
 int output_delta_blocks(int M, int N, int K) {
+  if (use_skinny(M, N, K)) return ((M + 63) / 64) * ((N + 31) / 32);
   if (choose_output_splits(M, N, K) > 1) return ((M + 127) / 128) * ((N + 63) / 64);
   return tile_count(M, N, K);
 }
@@ -768,6 +944,7 @@ int output_delta_splits(int M, int N, int K) { return choose_output_splits(M, N,
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
                          const float* bias, float* out, int ldo, const float* tab) {
   EpiSigmoid e{bias, out, ldo, tab};
+  if (use_skinny(M, N, K)) return launch_skinny<1, false>(s, A, lda, W, ldw, M, N, K, e);
   return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
 }
 
@@ -777,6 +954,7 @@ hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const fl
   const int sp = choose_output_splits(M, N, K);
   if (sp <= 1) {
     EpiOutputDelta e{bias, T, ldt, delta, ldd, sse_part, colsum, ldcs, tab, mask};
+    if (use_skinny(M, N, K)) return launch_skinny<2, false>(s, A, lda, W, ldw, M, N, K, e);
     return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
@@ -798,6 +976,7 @@ hipError_t output_finish(hipStream_t s, int M, int N, int K, const float* bias, 
 hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W, int ldw, int M, int N, int K,
                           const float* act, int lda, float* out, int ldo, float* colsum, int ldcs) {
   EpiHiddenDelta e{act, lda, out, ldo, colsum, ldcs};
+  if (use_skinny(M, N, K)) return launch_skinny<2, true>(s, D, ldd, W, ldw, M, N, K, e);
   return launch_cfg<false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 
