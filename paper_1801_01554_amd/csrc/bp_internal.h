@@ -50,6 +50,18 @@ int colsum_rows(int M);
 hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N,
                          int K, const float* bias, float* out, int ldo, const float* tab);
 
+// The first layer of an Elman step with its input built in the product
+// (section 10.5): A[m][k] = X[m][k] (X rows n_ext wide) for k < n_ext and
+// cont[m] H[m][k - n_ext] for k in [n_ext, K), H the previous step's first
+// hidden layer, whose first K - n_ext units the context copies in order;
+// out = sigma(A W + bias) as forward_layer.  rows_out (or nullptr) receives
+// A, with zeros in [K, ld_rows).  Only for forward_ctx_fits(M, N, K);
+// otherwise, or for a missing pointer, hipErrorInvalidValue.
+bool forward_ctx_fits(int M, int N, int K);
+hipError_t forward_ctx_layer(hipStream_t s, const float* X, int n_ext, const float* H, int ldh, const float* cont,
+                             const float* W, int ldw, int M, int N, int K, const float* bias, float* out, int ldo,
+                             float* rows_out, int ld_rows, const float* tab);
+
 // Output layer during training: y = sigma(A W + bias); e = (T - y) * mask[m]
 // (mask == nullptr: no mask);
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of

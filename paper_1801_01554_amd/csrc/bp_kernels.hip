@@ -491,20 +491,37 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 // 16 steps at a time with the next 32 in flight.  The four K partials of a
 // row block are added through LDS in K order, and the four waves of the row
 // block share its epilogue (RB = 2 for epilogues with 64-row column sums).
+//
+// With CTX, A is the input of an Elman step built on the fly (section 10.5):
+// A[m][k] = X[m][k] for k < n_ext, cont[m] H[m][k - n_ext] for the context
+// units, H being the previous step's first hidden layer (the context copies
+// its units in order).  The blocks of the first column strip also write the
+// rows they built to `out` (zeros in [K, ldo)), which the window's change
+// product reads.
 constexpr int kSkinnyChunk = 16;   // MFMA steps per load round
 
 inline bool use_skinny(int M, int N, int K) { return K <= 2048 && tiles_of(M, N, 64) < 128; }
 
-template <int RB, bool B_NK, bool AVEC, bool BVEC, class Epi>
+struct CtxInput {
+  const float* H = nullptr;   // previous step's hidden rows [M][ldh]
+  int ldh = 0;
+  const float* cont = nullptr;
+  int n_ext = 0;              // X = A, rows [M][lda]
+  float* out = nullptr;       // built rows [M][ldo], or nullptr
+  int ldo = 0;
+};
+
+template <int RB, bool B_NK, bool AVEC, bool BVEC, bool CTX, class Epi>
 __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restrict__ A, int lda,
                                                           const float* __restrict__ B, int ldb, int M, int N,
-                                                          int K, Epi epi) {
+                                                          int K, Epi epi, CtxInput ctx) {
   static_assert(!Epi::kFaults, "update epilogues take gemm_kernel");
   static_assert(!Epi::kColSum || RB == 2, "64-row column sums need RB = 2");
   constexpr int C = kSkinnyChunk;
   __shared__ float part[4][RB][16][64];
-  const int tiles_n = (N + 31) / 32;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+  const int tiles_m = (M + 32 * RB - 1) / (32 * RB), tiles_n = (N + 31) / 32;
+  int tm, tn;
+  xcd_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * 32 * RB, n0 = tn * 32;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rb = wave % RB, kg = wave / RB;
@@ -514,6 +531,9 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
   const int m = m0 + rb * 32 + r, n = n0 + r;        // A row and B column of this lane
   const int mc = min(m, M - 1), nc = min(n, N - 1);
   const float* arow = A + (size_t)mc * lda;
+  const float* hrow = CTX ? ctx.H + (size_t)mc * ctx.ldh : nullptr;
+  const float cm = CTX ? ctx.cont[mc] : 1.f;
+  const bool store_rows = CTX && ctx.out && tn == 0 && m < M;
 
   // operands of MFMA steps c C .. c C + C - 1 (zero past K, M or N).  Every
   // load reads a clamped, valid address and is issued before any mask is
@@ -524,7 +544,31 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
   auto masked = [](float v, int keep) { return __builtin_bit_cast(float, __builtin_bit_cast(int, v) & keep); };
   auto load = [&](int c, float* a, float* b) {
     const int k0 = kbase + c * C;
-    if (AVEC) {
+    if (CTX && AVEC) {
+      // n_ext % 4 == 0: each 4-vector lies in X or in H
+      f32x4 v[C / 4];
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q) {
+        const int k = k0 + 4 * q;
+        const float* p = k < ctx.n_ext ? arow + k : hrow + min(k - ctx.n_ext, ctx.ldh - 4);
+        v[q] = *reinterpret_cast<const f32x4*>(p);
+      }
+#pragma unroll
+      for (int q = 0; q < C / 4; ++q) {
+        const float sc = k0 + 4 * q < ctx.n_ext ? 1.f : cm;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e] * sc, k0 + 4 * q + e < K ? mrow : 0);
+      }
+    } else if (CTX) {
+#pragma unroll
+      for (int i = 0; i < C; ++i) {
+        const int k = k0 + i;
+        const float* p = k < ctx.n_ext ? arow + k : hrow + min(k - ctx.n_ext, ctx.ldh - 1);
+        a[i] = *p;
+      }
+#pragma unroll
+      for (int i = 0; i < C; ++i) a[i] = masked(a[i] * (k0 + i < ctx.n_ext ? 1.f : cm), k0 + i < K ? mrow : 0);
+    } else if (AVEC) {
       f32x4 v[C / 4];
 #pragma unroll
       for (int q = 0; q < C / 4; ++q) v[q] = *reinterpret_cast<const f32x4*>(arow + min(k0 + 4 * q, lda - 4));
@@ -564,7 +608,22 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
   // MFMA)
   const int nchunk = kh / C;
   float a0[C], b0[C], a1[C], b1[C], a2[C], b2[C];
-  auto mfma = [&](const float* a, const float* b) {
+  auto mfma = [&](int c, const float* a, const float* b) {
+    if (store_rows) {
+      // the built row segment, once the chunk's operands are in registers
+      const int k0 = kbase + c * C;
+      float* o = ctx.out + (size_t)m * ctx.ldo + k0;
+      if (AVEC) {
+#pragma unroll
+        for (int q = 0; q < C / 4; ++q)
+          if (k0 + 4 * q < ctx.ldo)
+            *reinterpret_cast<f32x4*>(o + 4 * q) = f32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
+      } else {
+#pragma unroll
+        for (int i = 0; i < C; ++i)
+          if (k0 + i < ctx.ldo) o[i] = a[i];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < C; ++i) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[i], acc, 0, 0, 0);
   };
@@ -572,13 +631,13 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
   if (nchunk > 1) load(1, a1, b1);
   for (int c = 0; c < nchunk; c += 3) {
     if (c + 2 < nchunk) load(c + 2, a2, b2);
-    mfma(a0, b0);
+    mfma(c, a0, b0);
     if (c + 1 >= nchunk) break;
     if (c + 3 < nchunk) load(c + 3, a0, b0);
-    mfma(a1, b1);
+    mfma(c + 1, a1, b1);
     if (c + 2 >= nchunk) break;
     if (c + 4 < nchunk) load(c + 4, a1, b1);
-    mfma(a2, b2);
+    mfma(c + 2, a2, b2);
   }
 
   // The K partials go through LDS; wave (rb, kg) then adds, in K-group
@@ -636,20 +695,27 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
   }
 }
 
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 template <int RB, bool B_NK, class Epi>
 hipError_t launch_skinny(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
                          const Epi& epi) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const int tiles = ((M + 32 * RB - 1) / (32 * RB)) * ((N + 31) / 32);
-  const bool avec = (lda % 4 == 0) && ((reinterpret_cast<uintptr_t>(A) & 15) == 0);
-  const bool bvec = B_NK && (ldb % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) & 15) == 0);
+  const bool avec = (lda % 4 == 0) && aligned16(A);
+  const bool bvec = B_NK && (ldb % 4 == 0) && aligned16(B);
+  const CtxInput none{};
   if (avec && bvec)
-    return launch_kernel(skinny_kernel<RB, B_NK, true, true, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+    return launch_kernel(skinny_kernel<RB, B_NK, true, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N,
+                         K, epi, none);
   if (avec)
-    return launch_kernel(skinny_kernel<RB, B_NK, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+    return launch_kernel(skinny_kernel<RB, B_NK, true, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M,
+                         N, K, epi, none);
   if (bvec)
-    return launch_kernel(skinny_kernel<RB, B_NK, false, true, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
-  return launch_kernel(skinny_kernel<RB, B_NK, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N, K, epi);
+    return launch_kernel(skinny_kernel<RB, B_NK, false, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M,
+                         N, K, epi, none);
+  return launch_kernel(skinny_kernel<RB, B_NK, false, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N,
+                       K, epi, none);
 }
 
 // --------------------------------------------------------------------------
@@ -946,6 +1012,28 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
   EpiSigmoid e{bias, out, ldo, tab};
   if (use_skinny(M, N, K)) return launch_skinny<1, false>(s, A, lda, W, ldw, M, N, K, e);
   return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
+}
+
+bool forward_ctx_fits(int M, int N, int K) { return use_skinny(M, N, K); }
+
+hipError_t forward_ctx_layer(hipStream_t s, const float* X, int n_ext, const float* H, int ldh, const float* cont,
+                             const float* W, int ldw, int M, int N, int K, const float* bias, float* out, int ldo,
+                             float* rows_out, int ld_rows, const float* tab) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (!use_skinny(M, N, K) || !H || !cont || n_ext < 0 || n_ext > K || (n_ext > 0 && !X) ||
+      ldh < K - n_ext || (rows_out && ld_rows < K))
+    return hipErrorInvalidValue;
+  EpiSigmoid e{bias, out, ldo, tab};
+  const CtxInput ctx{H, ldh, cont, n_ext, rows_out, ld_rows};
+  const float* A = n_ext > 0 ? X : H;   // X is not read when n_ext == 0
+  const int tiles = ((M + 31) / 32) * ((N + 31) / 32);
+  const bool avec = n_ext % 4 == 0 && aligned16(A) && ldh % 4 == 0 && aligned16(H) &&
+                    (!rows_out || (ld_rows % 4 == 0 && aligned16(rows_out)));
+  if (avec)
+    return launch_kernel(skinny_kernel<1, false, true, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W, ldw, M,
+                         N, K, e, ctx);
+  return launch_kernel(skinny_kernel<1, false, false, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W, ldw, M,
+                       N, K, e, ctx);
 }
 
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,

@@ -57,6 +57,7 @@ struct bp_net {
   // Elman context (section 10.5): context unit c (input n0 - n_ctx + c)
   // copies unit ctx_unit[c] of hidden layer ctx_layer[c]
   int n_ctx = 0;
+  bool ctx_in_order = false;          // ctx_layer[c] == 1 and ctx_unit[c] == c for every c
   int32_t* ctx_layer_dev = nullptr;
   int32_t* ctx_unit_dev = nullptr;
   float* seq_in = nullptr;            // assembled input rows of a window [rows][lda[0]]
@@ -266,6 +267,12 @@ struct BatchInput {
   int ldx = 0;                    // row stride of x (0: n0)
   const int32_t* act = nullptr;   // one-hot [rows][n_active]
   int n_active = 0;
+  // An Elman step whose input rows the first product builds: x holds the
+  // external inputs (ldx = n_ext), ctx_h the previous step's first hidden
+  // layer, cont the flags; the built rows go to rows_out (or nowhere).
+  const float* ctx_h = nullptr;
+  const float* cont = nullptr;
+  float* rows_out = nullptr;
 };
 
 int ldx_of(const bp_net* net, const BatchInput& in) { return in.ldx > 0 ? in.ldx : net->n[0]; }
@@ -294,6 +301,13 @@ int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, dou
       BP_LAUNCH(net, BP_K_GATHER,
                 bpk::onehot_forward(s, in.act, in.n_active, rows, wl(net, 0), net->ldw[0], net->n[0], net->n[1],
                                     (last && T) ? 1 : 0, dst, ldd, T, net->n[L], sse_part, net->sig_tab));
+      continue;
+    }
+    if (l == 0 && in.ctx_h) {
+      BP_LAUNCH(net, BP_K_FORWARD,
+                bpk::forward_ctx_layer(s, in.x, in.ldx, in.ctx_h, net->lda[1], in.cont, wl(net, 0), net->ldw[0], rows,
+                                       net->n[1], net->n[0], wbias(net, 0), dst, ldd, in.rows_out, net->lda[0],
+                                       net->sig_tab));
       continue;
     }
     const float* A = (l == 0) ? in.x : acts[l];
@@ -511,6 +525,25 @@ bpk::CtxSource ctx_source(bp_net* net, int64_t step, int S) {
   return src;
 }
 
+// The first product builds a step's input rows itself when the context
+// copies hidden layer 1 in order and the product takes the skinny kernel.
+bool fuse_ctx_input(const bp_net* net, int S) {
+  return net->ctx_in_order && bpk::forward_ctx_fits(S, net->n[1], net->n[0]);
+}
+
+// Input of a step whose first product builds the rows: external inputs of
+// the step, the context source `step` (S rows of hidden layer 1), the flags,
+// and where the built rows go.
+BatchInput ctx_input(bp_net* net, const float* X, int n_ext, const float* cont, int64_t step, int S, float* rows_out) {
+  BatchInput in;
+  in.x = n_ext > 0 ? X : nullptr;
+  in.ldx = n_ext;
+  in.ctx_h = net->act[1] + (size_t)step * S * net->lda[1];
+  in.cont = cont;
+  in.rows_out = rows_out;
+  return in;
+}
+
 int ensure_seq_in(bp_net* net, int64_t rows) {
   const size_t need = (size_t)rows * net->lda[0];
   if (need <= net->seq_in_cap) return BP_OK;
@@ -547,6 +580,7 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
   rc = ensure_sse(net, (size_t)T * per_step);
   if (rc) return rc;
   hipStream_t s = net->stream;
+  const bool fuse_ctx = fuse_ctx_input(net, S);
   std::vector<float*> acts(L + 1, nullptr);
   size_t used = 0;
   for (int64_t w0 = 0; w0 < T; w0 += B) {
@@ -557,12 +591,19 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
       // the previous (full) window, or none at the first step of the call
       const int64_t prev = k > 0 ? k - 1 : (w0 > 0 ? B - 1 : -1);
       float* A0 = net->seq_in + (size_t)k * S * net->lda[0];
-      BP_LAUNCH(net, BP_K_SEQ_IN,
-                bpk::seq_assemble(s, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
-                                  net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, prev, S), A0, net->lda[0]));
       BatchInput in;
-      in.x = A0;
-      in.ldx = net->lda[0];
+      // (with one step per window the source rows are the ones this step
+      // writes: those steps build the rows first)
+      if (fuse_ctx && prev >= 0 && prev != k) {
+        in = ctx_input(net, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, prev, S, A0);
+      } else {
+        BP_LAUNCH(net, BP_K_SEQ_IN,
+                  bpk::seq_assemble(s, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
+                                    net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, prev, S), A0,
+                                    net->lda[0]));
+        in.x = A0;
+        in.ldx = net->lda[0];
+      }
       for (int l = 1; l < L; ++l) acts[l] = net->act[l] + (size_t)k * S * net->lda[l];
       OutputView ov;
       ov.delta = net->del[L] + (size_t)k * S * net->lda[L];
@@ -596,16 +637,21 @@ int forward_sequences(bp_net* net, const float* X, const float* cont, int64_t T,
   if (rc) return rc;
   rc = ensure_seq_in(net, S);
   if (rc) return rc;
+  const bool fuse_ctx = fuse_ctx_input(net, S);
   std::vector<float*> acts(L + 1, nullptr);
   for (int64_t g = 0; g < T; ++g) {
     const int64_t half = g & 1;
-    BP_LAUNCH(net, BP_K_SEQ_IN,
-              bpk::seq_assemble(net->stream, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
-                                net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, g > 0 ? 1 - half : -1, S),
-                                net->seq_in, net->lda[0]));
     BatchInput in;
-    in.x = net->seq_in;
-    in.ldx = net->lda[0];
+    if (fuse_ctx && g > 0) {
+      in = ctx_input(net, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, 1 - half, S, nullptr);
+    } else {
+      BP_LAUNCH(net, BP_K_SEQ_IN,
+                bpk::seq_assemble(net->stream, X + (size_t)g * S * n_ext, n_ext, cont + (size_t)g * S, S, net->n_ctx,
+                                  net->ctx_layer_dev, net->ctx_unit_dev, ctx_source(net, g > 0 ? 1 - half : -1, S),
+                                  net->seq_in, net->lda[0]));
+      in.x = net->seq_in;
+      in.ldx = net->lda[0];
+    }
     for (int l = 1; l < L; ++l) acts[l] = net->act[l] + (size_t)half * S * net->lda[l];
     rc = run_forward(net, in, S, nullptr, nullptr, out + (size_t)g * S * nL, nL, acts.data());
     if (rc) return rc;
@@ -907,6 +953,7 @@ int bp_set_context(bp_net* net, int32_t n_ctx, const int32_t* from_layer, const 
   free_ptr(net->ctx_unit_dev);
   net->ctx_layer_dev = net->ctx_unit_dev = nullptr;
   net->n_ctx = 0;
+  net->ctx_in_order = false;
   if (n_ctx > 0) {
     BP_HIP(net, hipMalloc(&net->ctx_layer_dev, sizeof(int32_t) * n_ctx));
     BP_HIP(net, hipMalloc(&net->ctx_unit_dev, sizeof(int32_t) * n_ctx));
@@ -914,6 +961,9 @@ int bp_set_context(bp_net* net, int32_t n_ctx, const int32_t* from_layer, const 
     BP_HIP(net, hipMemcpy(net->ctx_unit_dev, from_unit, sizeof(int32_t) * n_ctx, hipMemcpyHostToDevice));
   }
   net->n_ctx = n_ctx;
+  net->ctx_in_order = n_ctx > 0;
+  for (int c = 0; c < n_ctx; ++c)
+    if (from_layer[c] != 1 || from_unit[c] != c) net->ctx_in_order = false;
   return BP_OK;
 }
 

@@ -174,3 +174,36 @@ def test_sequence_arguments_are_checked(dev):
     L = bp.lib()
     assert L.bp_train_sequences(net._h, None, None, None, None, 3, 4, 1, 0.1, 0.9, None) == bp.BP_EINVAL
     assert L.bp_train_sequences(net._h, None, None, None, None, 0, 0, 1, 0.1, 0.9, None) == bp.BP_EINVAL
+
+
+# Context copying hidden layer 1 in order: the first product builds the step's
+# input rows itself.  Cases: external inputs not a multiple of 4 wide (scalar
+# loads), one step per window (the source rows are the ones the step writes:
+# those steps build the rows first), no external input, and a context of the
+# first 24 of 40 hidden units.
+BUILT_INPUT_SPECS = [
+    wl.SeqSpec("elman-built-13+40", 13, (40,), 9, 40, 70, 23, 4, 3, 9, 0.01, 0.9, 2, 31),
+    wl.SeqSpec("elman-built-1-step", 16, (40,), 9, 40, 70, 11, 1, 3, 9, 0.01, 0.9, 2, 32),
+    wl.SeqSpec("elman-built-0+40", 0, (40,), 9, 40, 70, 17, 4, 3, 9, 0.01, 0.9, 2, 33),
+    wl.SeqSpec("elman-built-8+24of40", 8, (40, 16), 9, 24, 70, 17, 5, 3, 9, 0.01, 0.9, 2, 34),
+]
+
+
+@pytest.mark.parametrize("spec", BUILT_INPUT_SPECS, ids=lambda s: s.name)
+def test_input_built_in_product_matches_oracle(dev, spec):
+    w = wl.make_sequences(spec)
+    _say(f"case elman input built in product {spec.name}: sizes={w.sizes} window={spec.steps_per_update}")
+    net, o = _pair(w)
+    for e in range(spec.epochs):
+        sg, so = _both(net, o, w, dev)
+        _say(f"  epoch {e}: sse gpu {sg} oracle {so} rel {rel(sg, so):.3g}")
+        assert rel(sg, so) <= SSE_TOL
+    ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
+    _say(f"  weights rel err {ew}")
+    assert max(ew) <= 10 * W_TOL
+    x, _, c, _ = _dev_arrays(w, dev)
+    y = net.forward_sequences(x, c).cpu().numpy()
+    ref = o.forward_sequences(w.inputs, w.cont)
+    err = float(np.max(np.abs(y - ref)))
+    _say(f"  forward max abs err {err}")
+    assert err <= FWD_TOL
