@@ -46,12 +46,12 @@ PAPER_GF11_CPS = 9.01e8     # section 6.3, Table 1: 356 processors, tree summati
 PRIMARY = "nettalk-120-b512"
 SECONDARY = ("wide-1024-4096-1024", "deep-512-2048x3-64")
 SECONDARY_SEQ = ("elman-64+256-256-64",)
-GEMM_KINDS = ("forward", "output", "backward", "change")
+GEMM_KINDS = ("forward", "output", "backward", "change", "seq_pair")
 KERNEL_NAMES = {
-    "forward": "gemm_kernel<..., EpiSigmoid>",
-    "output": "gemm_kernel<..., EpiOutputDelta>",
-    "backward": "gemm_kernel<..., EpiHiddenDelta>",
-    "change": "gemm_kernel<..., EpiUpdate|EpiPartial>",
+    "forward": "gemm_kernel|skinny_kernel<..., EpiSigmoid>",
+    "output": "gemm_kernel|skinny_kernel<..., EpiOutputDelta>",
+    "backward": "gemm_kernel|skinny_kernel<..., EpiHiddenDelta>",
+    "change": "gemm_kernel|skinny_kernel<..., EpiUpdate|EpiPartial>",
     "splitk": "splitk_update_kernel",
     "bias": "bias_update_kernel",
     "gather": "onehot_forward_kernel",
@@ -61,6 +61,7 @@ KERNEL_NAMES = {
     "fused_update": "small_update_kernel",
     "output_finish": "output_finish_kernel",
     "seq_in": "seq_assemble_kernel",
+    "seq_pair": "elman_pair_kernel",
 }
 SMALL_MAX_HIDDEN, SMALL_MAX_OUT, SMALL_MAX_ACTIVE = 256, 64, 32   # the library's fused-path limits
 
@@ -110,15 +111,35 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
     return w
 
 
-def seq_kind_work(sizes, n_ctx, S, steps, splits_of):
+def seq_kind_work(sizes, n_ctx, S, steps, splits_of, built_steps=0, paired=False):
     """Algorithmic (flops, HBM bytes) per kind of one Elman window: `steps` forward steps of S
-    patterns (with the input assembly), then one backward pass and update over steps x S rows."""
+    patterns, then one backward pass and update over steps x S rows.  `built_steps` of the steps
+    have their input rows built by the first product (reading the flags besides X and the context
+    source, writing the rows); the others assemble them first (seq_in).  `paired`: steps 1 ..
+    steps - 1 run their hidden layer in one launch with the output layer of the step before
+    (seq_pair); the first step's hidden layer and the last step's output layer run alone."""
     n_ext = sizes[0] - n_ctx
-    w = {"seq_in": (0.0, 4.0 * steps * S * (n_ext + 1 + n_ctx + -(-sizes[0] // 4) * 4))}
-    for _ in range(steps):
-        for k, (f, b) in kind_work(sizes, S, False, 0, splits_of, ("fwd",)).items():
-            f0, b0 = w.get(k, (0.0, 0.0))
-            w[k] = (f0 + f, b0 + b)
+    rows_bytes = 4.0 * S * (1 + -(-sizes[0] // 4) * 4)          # flags read, rows written
+    w = {"seq_in": (0.0, (steps - built_steps) * (4.0 * S * (n_ext + n_ctx) + rows_bytes))}
+
+    def add(kind, f, b):
+        f0, b0 = w.get(kind, (0.0, 0.0))
+        w[kind] = (f0 + f, b0 + b)
+
+    step = kind_work(sizes, S, False, 0, splits_of, ("fwd",))
+    if paired:
+        pairs = steps - 1
+        add("forward", *step["forward"])
+        add("forward", 0.0, (built_steps - pairs) * rows_bytes)
+        add("output", *step["output"])
+        add("seq_pair", pairs * (step["forward"][0] + step["output"][0]),
+            pairs * (step["forward"][1] + step["output"][1] + rows_bytes))
+    else:
+        if built_steps:
+            add("forward", 0.0, built_steps * rows_bytes)
+        for _ in range(steps):
+            for k, (f, b) in step.items():
+                add(k, f, b)
     for k, (f, b) in kind_work(sizes, steps * S, False, 0, splits_of, ("bwd",)).items():
         f0, b0 = w.get(k, (0.0, 0.0))
         w[k] = (f0 + f, b0 + b)
@@ -130,6 +151,30 @@ def choose_output_splits(M, N, K):
     K <= 2048 take the skinny kernel, unsplit), for work accounting only."""
     if K <= 2048 and -(-M // 64) * -(-N // 64) < 128:
         return 1
+    return choose_splits(M, N, K)
+
+
+def input_built_in_product(sizes, n_ctx, S):
+    """Mirror of the library's choice to build an Elman step's input rows in the first product
+    (context copying hidden layer 1 in order, product on the skinny kernel)."""
+    return n_ctx > 0 and sizes[0] <= 2048 and -(-S // 64) * -(-sizes[1] // 64) < 128
+
+
+def elman_pair(sizes, n_ctx, S):
+    """Mirror of the library's choice to run an Elman step's hidden layer in one launch with the
+    output layer of the step before (one hidden layer, both products on the skinny kernel)."""
+    return (len(sizes) == 3 and input_built_in_product(sizes, n_ctx, S) and sizes[1] <= 2048
+            and -(-S // 64) * -(-sizes[2] // 64) < 128)
+
+
+def change_splits(M, N, K):
+    """Mirror of the library's split count for a change product, for work accounting only."""
+    if K >= 1024 and -(-M // 64) * -(-N // 64) < 128:
+        tiles, chunk = -(-M // 64) * -(-N // 32), 1024
+        while chunk > 128 and tiles * -(-K // chunk) < 512:
+            chunk //= 2
+        if -(-K // chunk) >= 2:
+            return -(-K // chunk)
     return choose_splits(M, N, K)
 
 
@@ -218,7 +263,7 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None)
     flops_step = sum(metrics.dense_flops_per_pattern(w.sizes, r) * r for r in step_rows(spec, calls))
     work = {}
     for r in step_rows(spec, calls):
-        for k, (f, b) in kind_work(w.sizes, r, w.active is not None, 7, choose_splits).items():
+        for k, (f, b) in kind_work(w.sizes, r, w.active is not None, 7, change_splits).items():
             f0, b0 = work.get(k, (0.0, 0.0))
             work[k] = (f0 + f, b0 + b)
     kernels, roof, gemm_f, gemm_ms = summarize_kernels(rep, work, name)
@@ -299,9 +344,13 @@ def run_seq_workload(name, epochs, torch, bp, wl, metrics, log):
     net.profile(False)
     net.close()
     work = {}
+    built = input_built_in_product(w.sizes, spec.n_ctx, spec.n_streams) and spec.steps_per_update > 1
     for w0 in range(0, spec.n_steps, spec.steps_per_update):
         steps = min(spec.steps_per_update, spec.n_steps - w0)
-        for k, (f, b) in seq_kind_work(w.sizes, spec.n_ctx, spec.n_streams, steps, choose_splits).items():
+        nb = (steps - 1 if w0 == 0 else steps) if built else 0     # one call per epoch: its first step assembles
+        paired = built and elman_pair(w.sizes, spec.n_ctx, spec.n_streams)
+        for k, (f, b) in seq_kind_work(w.sizes, spec.n_ctx, spec.n_streams, steps, change_splits, nb,
+                                       paired).items():
             f0, b0 = work.get(k, (0.0, 0.0))
             work[k] = (f0 + epochs * f, b0 + epochs * b)
     kernels, roof, gemm_f, gemm_ms = summarize_kernels(rep, work, name)
@@ -355,9 +404,10 @@ def kind_of_kernel(name):
             return "change" if m.group(1) == "true" else "output"
         return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
                 "EpiUpdate": "change"}.get(epi)
-    m = re.search(r"skinny_kernel<\d+, (true|false), (true|false), (true|false), [^>]*?(\w+)>", name)
+    m = re.search(r"skinny_kernel<\d+, [^>]*?(\w+)>", name)
     if m:
-        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward"}.get(m.group(4))
+        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
+                "EpiPartial": "change"}.get(m.group(1))
     for k, v in KERNEL_NAMES.items():
         if "<" not in v and v in name:
             return k

@@ -228,7 +228,8 @@ enum {
   BP_K_FUSED_UPD = 10,/* small one-hot nets: both layers' change + update   */
   BP_K_OUTFIN = 11,   /* split-K output layer: partial sums + deltas + error */
   BP_K_SEQ_IN = 12,   /* Elman nets: input rows of a step with the context copy */
-  BP_K_COUNT = 13
+  BP_K_SEQ_PAIR = 13, /* Elman nets: hidden layer of a step + output layer of the step before */
+  BP_K_COUNT = 14
 };
 
 /* Graph replay of repeated training calls (on by default).  With on != 0,

@@ -62,6 +62,20 @@ hipError_t forward_ctx_layer(hipStream_t s, const float* X, int n_ext, const flo
                              const float* W, int ldw, int M, int N, int K, const float* bias, float* out, int ldo,
                              float* rows_out, int ld_rows, const float* tab);
 
+// An Elman net with one hidden layer: step t + 1's hidden layer (as
+// forward_ctx_layer, from Hprev = step t's hidden rows into Hnext, rows built
+// into rows_out or nowhere) and step t's output layer with its deltas (as
+// forward_output_delta with A = Hprev) in one launch.  All hidden rows have
+// stride ldh.  Only for elman_pair_fits(S, n0, n1, n2) (then
+// output_delta_blocks(S, n2, n1) error partials); otherwise, or for a
+// missing pointer, hipErrorInvalidValue.
+bool elman_pair_fits(int S, int n0, int n1, int n2);
+hipError_t elman_pair(hipStream_t s, const float* X, int n_ext, const float* Hprev, const float* cont,
+                      const float* W0, int ldw0, const float* bias0, int n0, int n1, float* Hnext, float* rows_out,
+                      int ld_rows, const float* W1, int ldw1, const float* bias1, int n2, int ldh, int S,
+                      const float* T, int ldt, float* delta, int ldd, double* sse_part, float* colsum, int ldcs,
+                      const float* tab, const float* mask);
+
 // Output layer during training: y = sigma(A W + bias); e = (T - y) * mask[m]
 // (mask == nullptr: no mask);
 // delta[m][n] = e y (1 - y); sse_part[b] = sum of e^2 over the elements of

@@ -14,6 +14,8 @@
 // Every reduction runs in a fixed order: results are run-to-run identical.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "bp_device.h"
 #include "bp_internal.h"
 
@@ -492,6 +494,14 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 // row block are added through LDS in K order, and the four waves of the row
 // block share its epilogue (RB = 2 for epilogues with 64-row column sums).
 //
+// With EpiPartial the kernel is a split-K change product (section 6.2.1, the
+// batch-summed change of one layer's weights when the batch is long and the
+// layer small): A is stored k-major (A[k][m], the activations), the block
+// covers K range [z k_chunk, (z + 1) k_chunk) of split z and writes raw
+// partial sums for splitk_finish.  Blocks are ordered split-major and handed
+// to the XCDs in contiguous ranges, so each XCD reads one K range of both
+// operands.
+//
 // With CTX, A is the input of an Elman step built on the fly (section 10.5):
 // A[m][k] = X[m][k] for k < n_ext, cont[m] H[m][k - n_ext] for the context
 // units, H being the previous step's first hidden layer (the context copies
@@ -511,23 +521,38 @@ struct CtxInput {
   int ldo = 0;
 };
 
-template <int RB, bool B_NK, bool AVEC, bool BVEC, bool CTX, class Epi>
-__global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restrict__ A, int lda,
-                                                          const float* __restrict__ B, int ldb, int M, int N,
-                                                          int K, Epi epi, CtxInput ctx) {
+// The work of block `bid` of `nblocks` (a kernel may give a range of its
+// blocks to each of several products); `part` is the block's LDS for the K
+// partials.
+template <int RB, bool A_KM, bool B_NK, bool AVEC, bool BVEC, bool CTX, class Epi>
+__device__ __forceinline__ void skinny_body(int bid, int nblocks, float (&part)[4][RB][16][64],
+                                            const float* __restrict__ A, int lda, const float* __restrict__ B,
+                                            int ldb, int M, int N, int K, int k_chunk, const Epi& epi,
+                                            const CtxInput& ctx) {
+  constexpr bool SPLIT = std::is_same_v<Epi, EpiPartial>;
   static_assert(!Epi::kFaults, "update epilogues take gemm_kernel");
   static_assert(!Epi::kColSum || RB == 2, "64-row column sums need RB = 2");
+  static_assert(!A_KM || (SPLIT && !AVEC && !CTX), "k-major A is the change product's");
   constexpr int C = kSkinnyChunk;
-  __shared__ float part[4][RB][16][64];
   const int tiles_m = (M + 32 * RB - 1) / (32 * RB), tiles_n = (N + 31) / 32;
-  int tm, tn;
-  xcd_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  int tm, tn, z = 0;
+  if constexpr (SPLIT) {
+    const int per = nblocks >> 3;
+    const int t = bid >= (per << 3) ? bid : (bid & 7) * per + (bid >> 3);
+    const int tiles = tiles_m * tiles_n;
+    z = t / tiles;
+    tm = (t - z * tiles) / tiles_n;
+    tn = t - z * tiles - tm * tiles_n;
+  } else {
+    xcd_tile(bid, nblocks, tiles_m, tiles_n, tm, tn);
+  }
+  const int kstart = z * k_chunk, kend = min(K, kstart + k_chunk);
   const int m0 = tm * 32 * RB, n0 = tn * 32;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rb = wave % RB, kg = wave / RB;
   const int r = lane & 31, h = lane >> 5;
-  const int kh = ((K + 7) / 8 + C - 1) / C * C;      // KH
-  const int kbase = kg * 2 * kh + h * kh;            // this lane's first k
+  const int kh = ((kend - kstart + 7) / 8 + C - 1) / C * C;   // KH
+  const int kbase = kstart + kg * 2 * kh + h * kh;            // this lane's first k
   const int m = m0 + rb * 32 + r, n = n0 + r;        // A row and B column of this lane
   const int mc = min(m, M - 1), nc = min(n, N - 1);
   const float* arow = A + (size_t)mc * lda;
@@ -557,7 +582,7 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
       for (int q = 0; q < C / 4; ++q) {
         const float sc = k0 + 4 * q < ctx.n_ext ? 1.f : cm;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e] * sc, k0 + 4 * q + e < K ? mrow : 0);
+        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e] * sc, k0 + 4 * q + e < kend ? mrow : 0);
       }
     } else if (CTX) {
 #pragma unroll
@@ -567,7 +592,12 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
         a[i] = *p;
       }
 #pragma unroll
-      for (int i = 0; i < C; ++i) a[i] = masked(a[i] * (k0 + i < ctx.n_ext ? 1.f : cm), k0 + i < K ? mrow : 0);
+      for (int i = 0; i < C; ++i) a[i] = masked(a[i] * (k0 + i < ctx.n_ext ? 1.f : cm), k0 + i < kend ? mrow : 0);
+    } else if (A_KM) {
+#pragma unroll
+      for (int i = 0; i < C; ++i) a[i] = A[(size_t)min(k0 + i, K - 1) * lda + mc];
+#pragma unroll
+      for (int i = 0; i < C; ++i) a[i] = masked(a[i], k0 + i < kend ? mrow : 0);
     } else if (AVEC) {
       f32x4 v[C / 4];
 #pragma unroll
@@ -575,12 +605,12 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
 #pragma unroll
       for (int q = 0; q < C / 4; ++q)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < K ? mrow : 0);
+        for (int e = 0; e < 4; ++e) a[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < kend ? mrow : 0);
     } else {
 #pragma unroll
       for (int i = 0; i < C; ++i) a[i] = arow[min(k0 + i, K - 1)];
 #pragma unroll
-      for (int i = 0; i < C; ++i) a[i] = masked(a[i], k0 + i < K ? mrow : 0);
+      for (int i = 0; i < C; ++i) a[i] = masked(a[i], k0 + i < kend ? mrow : 0);
     }
     if (B_NK && BVEC) {
       const float* brow = B + (size_t)nc * ldb;
@@ -590,13 +620,13 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
 #pragma unroll
       for (int q = 0; q < C / 4; ++q)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) b[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < K ? ncol : 0);
+        for (int e = 0; e < 4; ++e) b[4 * q + e] = masked(v[q][e], k0 + 4 * q + e < kend ? ncol : 0);
     } else {
 #pragma unroll
       for (int i = 0; i < C; ++i)
         b[i] = B_NK ? B[(size_t)nc * ldb + min(k0 + i, K - 1)] : B[(size_t)min(k0 + i, K - 1) * ldb + nc];
 #pragma unroll
-      for (int i = 0; i < C; ++i) b[i] = masked(b[i], k0 + i < K ? ncol : 0);
+      for (int i = 0; i < C; ++i) b[i] = masked(b[i], k0 + i < kend ? ncol : 0);
     }
   };
 
@@ -662,7 +692,11 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int mm = m0 + rb * 32 + 8 * kg + 4 * h + q;
-      if (mm < M) csum += epi.apply(mm, n, v[q], cv, pre[q], sse);
+      if constexpr (SPLIT) {
+        if (mm < M) epi.P[z * epi.split_stride + (size_t)mm * epi.ldp + n] = v[q];
+      } else {
+        if (mm < M) csum += epi.apply(mm, n, v[q], cv, pre[q], sse);
+      }
     }
   }
   if constexpr (Epi::kColSum) {
@@ -690,9 +724,39 @@ __global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restric
     if (threadIdx.x == 0) {
       double s = 0.0;
       for (int w = 0; w < 4 * RB; ++w) s += (double)red[w];
-      epi.sse_part[blockIdx.x] = s;
+      epi.sse_part[bid] = s;
     }
   }
+}
+
+template <int RB, bool A_KM, bool B_NK, bool AVEC, bool BVEC, bool CTX, class Epi>
+__global__ __launch_bounds__(256 * RB) void skinny_kernel(const float* __restrict__ A, int lda,
+                                                          const float* __restrict__ B, int ldb, int M, int N,
+                                                          int K, int k_chunk, Epi epi, CtxInput ctx) {
+  __shared__ float part[4][RB][16][64];
+  skinny_body<RB, A_KM, B_NK, AVEC, BVEC, CTX>(blockIdx.x, gridDim.x, part, A, lda, B, ldb, M, N, K, k_chunk, epi,
+                                               ctx);
+}
+
+// Two independent products of an Elman net with one hidden layer in one
+// launch (section 10.5): the hidden layer of step t + 1 (input built in the
+// product) and the output layer of step t with its deltas, which both read
+// step t's hidden rows and nothing the other writes.  Blocks [0, nh) take
+// the first, the rest the second; 64 x 32 tiles for both.
+template <bool AVEC_H, bool AVEC_O>
+__global__ __launch_bounds__(512) void elman_pair_kernel(const float* __restrict__ X, int n_ext,
+                                                         const float* __restrict__ W0, int ldw0, int n0, int n1,
+                                                         EpiSigmoid eh, CtxInput ctx,
+                                                         const float* __restrict__ H, int ldh,
+                                                         const float* __restrict__ W1, int ldw1, int n2,
+                                                         EpiOutputDelta eo, int S, int nh) {
+  __shared__ float part[4][2][16][64];
+  if ((int)blockIdx.x < nh)
+    skinny_body<2, false, false, AVEC_H, false, true>(blockIdx.x, nh, part, X, n_ext, W0, ldw0, S, n1, n0, n0, eh,
+                                                      ctx);
+  else
+    skinny_body<2, false, false, AVEC_O, false, false>(blockIdx.x - nh, gridDim.x - nh, part, H, ldh, W1, ldw1, S, n2,
+                                                       n1, n1, eo, CtxInput{});
 }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -706,16 +770,16 @@ hipError_t launch_skinny(hipStream_t s, const float* A, int lda, const float* B,
   const bool bvec = B_NK && (ldb % 4 == 0) && aligned16(B);
   const CtxInput none{};
   if (avec && bvec)
-    return launch_kernel(skinny_kernel<RB, B_NK, true, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N,
-                         K, epi, none);
+    return launch_kernel(skinny_kernel<RB, false, B_NK, true, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb,
+                         M, N, K, K, epi, none);
   if (avec)
-    return launch_kernel(skinny_kernel<RB, B_NK, true, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M,
-                         N, K, epi, none);
+    return launch_kernel(skinny_kernel<RB, false, B_NK, true, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B,
+                         ldb, M, N, K, K, epi, none);
   if (bvec)
-    return launch_kernel(skinny_kernel<RB, B_NK, false, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M,
-                         N, K, epi, none);
-  return launch_kernel(skinny_kernel<RB, B_NK, false, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb, M, N,
-                       K, epi, none);
+    return launch_kernel(skinny_kernel<RB, false, B_NK, false, true, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B,
+                         ldb, M, N, K, K, epi, none);
+  return launch_kernel(skinny_kernel<RB, false, B_NK, false, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb,
+                       M, N, K, K, epi, none);
 }
 
 // --------------------------------------------------------------------------
@@ -729,8 +793,18 @@ __global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __
   int nf = 0;
   if (idx < (size_t)M * N) {
     const int m = (int)(idx / N), n = (int)(idx % N);
+    // eight partials in flight at a time, added in split order
+    const float* p = P + (size_t)m * ldp + n;
     float g = 0.f;
-    for (int z = 0; z < splits; ++z) g += P[z * split_stride + (size_t)m * ldp + n];
+    int z = 0;
+    for (; z + 8 <= splits; z += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p[(z + e) * split_stride];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) g += v[e];
+    }
+    for (; z < splits; ++z) g += p[z * split_stride];
     g = checked_change(g, limit, nf);
     const size_t i = (size_t)m * ldw + n;
     const float v = momentum_step(g, V[i], lr, mom);
@@ -1030,10 +1104,42 @@ hipError_t forward_ctx_layer(hipStream_t s, const float* X, int n_ext, const flo
   const bool avec = n_ext % 4 == 0 && aligned16(A) && ldh % 4 == 0 && aligned16(H) &&
                     (!rows_out || (ld_rows % 4 == 0 && aligned16(rows_out)));
   if (avec)
-    return launch_kernel(skinny_kernel<1, false, true, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W, ldw, M,
-                         N, K, e, ctx);
-  return launch_kernel(skinny_kernel<1, false, false, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W, ldw, M,
-                       N, K, e, ctx);
+    return launch_kernel(skinny_kernel<1, false, false, true, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W,
+                         ldw, M, N, K, K, e, ctx);
+  return launch_kernel(skinny_kernel<1, false, false, false, false, true, EpiSigmoid>, tiles, 256, 0, s, A, n_ext, W,
+                       ldw, M, N, K, K, e, ctx);
+}
+
+bool elman_pair_fits(int S, int n0, int n1, int n2) { return use_skinny(S, n1, n0) && use_skinny(S, n2, n1); }
+
+hipError_t elman_pair(hipStream_t s, const float* X, int n_ext, const float* Hprev, const float* cont,
+                      const float* W0, int ldw0, const float* bias0, int n0, int n1, float* Hnext, float* rows_out,
+                      int ld_rows, const float* W1, int ldw1, const float* bias1, int n2, int ldh, int S,
+                      const float* T, int ldt, float* delta, int ldd, double* sse_part, float* colsum, int ldcs,
+                      const float* tab, const float* mask) {
+  if (S <= 0 || n1 <= 0 || n2 <= 0) return hipSuccess;
+  if (!elman_pair_fits(S, n0, n1, n2) || !Hprev || !cont || !Hnext || n_ext < 0 || n_ext > n0 ||
+      (n_ext > 0 && !X) || ldh < n1 || (rows_out && ld_rows < n0))
+    return hipErrorInvalidValue;
+  const float* A = n_ext > 0 ? X : Hprev;   // X is not read when n_ext == 0
+  EpiSigmoid eh{bias0, Hnext, ldh, tab};
+  const CtxInput ctx{Hprev, ldh, cont, n_ext, rows_out, ld_rows};
+  EpiOutputDelta eo{bias1, T, ldt, delta, ldd, sse_part, colsum, ldcs, tab, mask};
+  const int nh = ((S + 63) / 64) * ((n1 + 31) / 32), no = ((S + 63) / 64) * ((n2 + 31) / 32);
+  const bool avh = n_ext % 4 == 0 && aligned16(A) && ldh % 4 == 0 && aligned16(Hprev) &&
+                   (!rows_out || (ld_rows % 4 == 0 && aligned16(rows_out)));
+  const bool avo = ldh % 4 == 0 && aligned16(Hprev);
+  if (avh && avo)
+    return launch_kernel(elman_pair_kernel<true, true>, nh + no, 512, 0, s, A, n_ext, W0, ldw0, n0, n1, eh, ctx, Hprev,
+                         ldh, W1, ldw1, n2, eo, S, nh);
+  if (avh)
+    return launch_kernel(elman_pair_kernel<true, false>, nh + no, 512, 0, s, A, n_ext, W0, ldw0, n0, n1, eh, ctx,
+                         Hprev, ldh, W1, ldw1, n2, eo, S, nh);
+  if (avo)
+    return launch_kernel(elman_pair_kernel<false, true>, nh + no, 512, 0, s, A, n_ext, W0, ldw0, n0, n1, eh, ctx,
+                         Hprev, ldh, W1, ldw1, n2, eo, S, nh);
+  return launch_kernel(elman_pair_kernel<false, false>, nh + no, 512, 0, s, A, n_ext, W0, ldw0, n0, n1, eh, ctx, Hprev,
+                       ldh, W1, ldw1, n2, eo, S, nh);
 }
 
 hipError_t forward_output_delta(hipStream_t s, const float* A, int lda, const float* W, int ldw, int M, int N, int K,
@@ -1068,10 +1174,33 @@ hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W
   return launch_cfg<false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 
-int change_splits(int M, int N, int K) { return choose_splits(M, N, K); }
+// The change product of a layer: few output tiles and a long batch take the
+// split-K skinny kernel (64 x 32 tiles), with the largest K chunk of 1024,
+// 512, 256 or 128 that still gives kSkinnyChangeBlocks blocks; the others
+// take gemm_kernel, split over K when the batch is long (choose_splits).
+constexpr int kSkinnyChangeBlocks = 512;
+struct ChangePlan {
+  bool skinny;
+  int splits;
+  int chunk;
+};
+
+ChangePlan change_plan(int M, int N, int K) {
+  if (K >= 1024 && tiles_of(M, N, 64) < 128) {
+    const long tiles = (long)((M + 63) / 64) * ((N + 31) / 32);
+    int chunk = 1024;
+    while (chunk > 128 && tiles * ((K + chunk - 1) / chunk) < kSkinnyChangeBlocks) chunk /= 2;
+    const int sp = (K + chunk - 1) / chunk;
+    if (sp >= 2) return {true, sp, chunk};
+  }
+  const int sp = choose_splits(M, N, K);
+  return {false, sp, sp > 1 ? chunk_for(K, sp) : K};
+}
+
+int change_splits(int M, int N, int K) { return change_plan(M, N, K).splits; }
 
 size_t change_update_workspace(int M, int N, int K) {
-  const int sp = choose_splits(M, N, K);
+  const int sp = change_splits(M, N, K);
   if (sp <= 1) return 0;
   const int ldp = (N + 3) / 4 * 4;
   return (size_t)sp * M * ldp;
@@ -1081,19 +1210,24 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
                          float* W, float* V, int ldw, float lr, float mom, float* ws, float limit,
                          unsigned long long* faults) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  const int sp = choose_splits(M, N, K);
-  if (sp <= 1) {
+  const ChangePlan pl = change_plan(M, N, K);
+  if (pl.splits <= 1) {
     EpiUpdate e{W, V, ldw, lr, mom, limit, faults};
     return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
   }
   const int ldp = (N + 3) / 4 * 4;
   EpiPartial e{ws, ldp, (size_t)M * ldp};
-  return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, sp, chunk_for(K, sp), e);
+  if (pl.skinny) {
+    const int blocks = ((M + 63) / 64) * ((N + 31) / 32) * pl.splits;
+    return launch_kernel(skinny_kernel<2, true, false, false, false, false, EpiPartial>, blocks, 512, 0, s, A, lda, D,
+                         ldd, M, N, K, pl.chunk, e, CtxInput{});
+  }
+  return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, pl.splits, pl.chunk, e);
 }
 
 hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
                          const float* ws, float limit, unsigned long long* faults) {
-  const int sp = choose_splits(M, N, K);
+  const int sp = change_splits(M, N, K);
   if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
   const int ldp = (N + 3) / 4 * 4;
   const size_t total = (size_t)M * N;

@@ -288,12 +288,13 @@ struct OutputView {
 // Forward pass of `rows` patterns; the last layer either applies the output
 // delta epilogue (training, T != nullptr) or writes sigma to `out`.
 int run_forward(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part,
-                float* out, int ldo, float* const* acts, OutputView ov = OutputView()) {
+                float* out, int ldo, float* const* acts, OutputView ov = OutputView(), int l_begin = 0,
+                int l_end = -1) {
   if (!ov.delta) ov.delta = net->del[net->L];
   if (!ov.csum) ov.csum = net->csum[net->L];
   const int L = net->L;
   hipStream_t s = net->stream;
-  for (int l = 0; l < L; ++l) {
+  for (int l = l_begin; l < (l_end < 0 ? L : l_end); ++l) {
     const bool last = (l == L - 1);
     float* dst = last ? (T ? ov.delta : out) : acts[l + 1];
     const int ldd = last ? (T ? net->lda[L] : ldo) : net->lda[l + 1];
@@ -581,12 +582,36 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
   if (rc) return rc;
   hipStream_t s = net->stream;
   const bool fuse_ctx = fuse_ctx_input(net, S);
+  // one hidden layer: step k's hidden layer and step k - 1's output layer
+  // share a launch; a window's first hidden layer and last output layer run
+  // alone
+  const bool pair = fuse_ctx && L == 2 && B > 1 && bpk::elman_pair_fits(S, net->n[0], net->n[1], net->n[2]);
+  const int lda1 = net->lda[1], ldL = net->lda[L];
   std::vector<float*> acts(L + 1, nullptr);
-  size_t used = 0;
+  // the output layer's view of step k of the window (step g of the call)
+  auto view = [&](int k, int64_t g) {
+    OutputView ov;
+    ov.delta = net->del[L] + (size_t)k * S * ldL;
+    ov.csum = net->csum[L] + (size_t)k * csS * ldL;
+    ov.mask = mask + (size_t)g * S;
+    return ov;
+  };
   for (int64_t w0 = 0; w0 < T; w0 += B) {
     const int steps = (int)std::min<int64_t>(B, T - w0);
     for (int k = 0; k < steps; ++k) {
       const int64_t g = w0 + k;
+      if (pair && k > 0) {
+        const OutputView ov = view(k - 1, g - 1);
+        const float* hp = net->act[1] + (size_t)(k - 1) * S * lda1;
+        BP_LAUNCH(net, BP_K_SEQ_PAIR,
+                  bpk::elman_pair(s, n_ext > 0 ? X + (size_t)g * S * n_ext : nullptr, n_ext, hp, cont + (size_t)g * S,
+                                  wl(net, 0), net->ldw[0], wbias(net, 0), net->n[0], net->n[1],
+                                  net->act[1] + (size_t)k * S * lda1, net->seq_in + (size_t)k * S * net->lda[0],
+                                  net->lda[0], wl(net, 1), net->ldw[1], wbias(net, 1), nL, lda1, S,
+                                  targets + (size_t)(g - 1) * S * nL, nL, ov.delta, ldL,
+                                  net->sse_part + (size_t)(g - 1) * per_step, ov.csum, ldL, net->sig_tab, ov.mask));
+        continue;
+      }
       // context source: the previous step of this window, or the last step of
       // the previous (full) window, or none at the first step of the call
       const int64_t prev = k > 0 ? k - 1 : (w0 > 0 ? B - 1 : -1);
@@ -605,13 +630,17 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
         in.ldx = net->lda[0];
       }
       for (int l = 1; l < L; ++l) acts[l] = net->act[l] + (size_t)k * S * net->lda[l];
-      OutputView ov;
-      ov.delta = net->del[L] + (size_t)k * S * net->lda[L];
-      ov.csum = net->csum[L] + (size_t)k * csS * net->lda[L];
-      ov.mask = mask + (size_t)g * S;
-      rc = run_forward(net, in, S, targets + (size_t)g * S * nL, net->sse_part + used, nullptr, 0, acts.data(), ov);
+      rc = run_forward(net, in, S, targets + (size_t)g * S * nL, net->sse_part + (size_t)g * per_step, nullptr, 0,
+                       acts.data(), view(k, g), 0, pair ? L - 1 : L);
       if (rc) return rc;
-      used += (size_t)per_step;
+    }
+    if (pair) {
+      const int k = steps - 1;
+      const int64_t g = w0 + k;
+      acts[1] = net->act[1] + (size_t)k * S * lda1;
+      rc = run_forward(net, BatchInput(), S, targets + (size_t)g * S * nL, net->sse_part + (size_t)g * per_step,
+                       nullptr, 0, acts.data(), view(k, g), L - 1, L);
+      if (rc) return rc;
     }
     BatchInput win;
     win.x = net->seq_in;
@@ -619,7 +648,7 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
     rc = run_backward_update(net, win, steps * S, lr, mom, steps * csS);
     if (rc) return rc;
   }
-  BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(s, net->sse_part, (int)used, net->sse_dev));
+  BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(s, net->sse_part, (int)(T * per_step), net->sse_dev));
   if (sse_out) {
     BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, s));
     BP_HIP(net, hipStreamSynchronize(s));

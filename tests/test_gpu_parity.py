@@ -124,6 +124,10 @@ def test_first_update_full_size(dev, name):
     ((203, 256, 64), 300, 100, True),     # fused path at its largest hidden and output sizes
     ((60, 1, 1), 40, 7, True),
     ((203, 257, 26), 70, 70, True),       # just past the fused path's hidden limit (generic path)
+    # long batches over small layers: split-K change products on the skinny kernel (ragged K, rows, columns)
+    ((97, 33, 3), 2500, 2500, False),
+    ((64, 200, 10), 4096, 4096, False),
+    ((1, 40, 1), 1500, 1500, False),
 ])
 def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
