@@ -239,7 +239,8 @@ enum {
  * arguments replay that graph instead of launching each kernel: same
  * kernels, same results bit for bit, less launch overhead per update.  A
  * change of workspace size, sigmoid mode or range check, or profiling,
- * drops back to direct launches.  The graph reads the argument buffers at
+ * drops back to direct launches.  Calls of a single batch always launch
+ * directly (a graph launch costs more host time than their few kernels).  The graph reads the argument buffers at
  * replay time, so their contents may change between calls.  on == 0: every
  * call launches directly.  Waits for the net's stream; drops any graph. */
 int bp_set_graph_replay(bp_net* net, int on);

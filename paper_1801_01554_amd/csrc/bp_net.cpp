@@ -476,7 +476,9 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
                       (size_t)sse_blocks(net, in, last_rows);
   rc = ensure_sse(net, need);
   if (rc) return rc;
-  if (net->graph_on && !net->prof) {
+  // A call of one batch launches directly: its three or so launches cost
+  // less host time than a graph launch.
+  if (net->graph_on && !net->prof && nb >= 2) {
     bp_net::TrainKey key;
     key.x = in.x;
     key.act = in.act;

@@ -8,7 +8,8 @@ Each case interleaves the replays with the program's own eager work (a
 forward pass, host copies, synchronisations), changes an argument (the
 learning rate: a new capture) and an option (the table sigmoid: the
 captured graph is dropped), and covers the fused small-net path, the dense
-generic path and the one-hot generic path.
+generic path and the one-hot generic path.  Calls of a single batch always
+launch directly; their case checks that the replay setting leaves them so.
 """
 import numpy as np
 import pytest
@@ -41,6 +42,7 @@ CASES = [
     ("fused small-net path", (203, 120, 26), 2048, 512, True),
     ("dense generic path", (64, 96, 10), 3000, 1024, False),
     ("one-hot generic path", (60, 40, 30, 12), 1500, 256, True),
+    ("single batch per call (direct launches)", (203, 120, 26), 512, 512, True),
 ]
 
 
