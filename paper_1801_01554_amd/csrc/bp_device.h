@@ -53,6 +53,31 @@ __device__ __forceinline__ float momentum_step(float g, float v_old, float lr, f
   return fmaf(lr, g, mom * v_old);
 }
 
+// The error of a training call (section 10.1 reports the total squared
+// error): out[0] = the sum of part[0, n) in double, in a fixed order (each of
+// the NT threads adds a strided subset, eight loads in flight, then a tree
+// over the threads).  Every thread of the NT-thread block must call it;
+// `red` is NT doubles of LDS.
+template <int NT>
+__device__ __forceinline__ void block_sum_partials(const double* __restrict__ part, int n, double* out,
+                                                   double* red) {
+  double s = 0.0;
+  for (int i0 = threadIdx.x; i0 < n; i0 += 8 * NT) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = i0 + u * NT < n ? part[i0 + u * NT] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = NT / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
 // Adds the fault counts of a wave to the device counter: a wave sum, then one
 // atomic from lane 0 when the sum is nonzero.  Every lane of the wave must
 // reach this call.

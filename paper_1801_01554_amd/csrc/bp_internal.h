@@ -162,10 +162,13 @@ hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int row
                         int H, const float* W1, int ldw1, int O, const float* T, float* A1q, float* D1, int ldd1,
                         float* D2, int ldd2, double* sse_part, const float* tab);
 
-// Summed changes of both layers over the batch and the momentum update of all weights.
+// Summed changes of both layers over the batch and the momentum update of all
+// weights.  With sse_out != nullptr (the last update of a call) one more
+// block writes the sum of sse_part[0, n_sse) to sse_out, as sse_reduce.
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1q, const float* D1,
                         int ldd1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults);
+                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults,
+                        const double* sse_part = nullptr, int n_sse = 0, double* sse_out = nullptr);
 
 // ---- Elman nets (bp_seq.hip, section 10.5)
 // Hidden layers a context unit may copy from: 1 .. kCtxMaxLayer.

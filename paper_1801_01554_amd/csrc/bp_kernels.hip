@@ -1020,21 +1020,7 @@ __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* 
 constexpr int kRed = 1024;
 __global__ __launch_bounds__(kRed) void sse_reduce_kernel(const double* __restrict__ part, int n, double* out) {
   __shared__ double red[kRed];
-  double s = 0.0;
-  for (int i0 = threadIdx.x; i0 < n; i0 += 8 * kRed) {
-    double v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = i0 + u * kRed < n ? part[i0 + u * kRed] : 0.0;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s += v[u];
-  }
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = kRed / 2; w > 0; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) out[0] = red[0];
+  block_sum_partials<kRed>(part, n, out, red);
 }
 
 // K-splits for a product with few output tiles: enough blocks for two per

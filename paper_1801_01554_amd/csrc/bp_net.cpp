@@ -342,7 +342,10 @@ int sse_blocks(const bp_net* net, const BatchInput& in, int rows) {
 }
 
 // One pooled update of a small one-hot two-layer net: two launches.
-int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part, float lr, float mom) {
+// The fused two-launch update of one batch; with n_sse >= 0 (the call's last
+// batch) the update launch also sums the call's n_sse error partials.
+int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, double* sse_part, float lr, float mom,
+              int n_sse = -1) {
   hipStream_t s = net->stream;
   const int n0 = net->n[0], H = net->n[1], O = net->n[2];
   BP_LAUNCH(net, BP_K_FUSED_FB,
@@ -352,7 +355,8 @@ int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, doubl
   BP_LAUNCH(net, BP_K_FUSED_UPD,
             bpk::small_update(s, in.act, in.n_active, rows, net->splitk, net->del[1], net->lda[1], net->del[2],
                               net->lda[2], wl(net, 0), vl(net, 0), net->ldw[0], n0, H, wl(net, 1), vl(net, 1),
-                              net->ldw[1], O, lr, mom, net->fault_limit, net->faults));
+                              net->ldw[1], O, lr, mom, net->fault_limit, net->faults, net->sse_part, n_sse,
+                              n_sse >= 0 ? net->sse_dev : nullptr));
   return BP_OK;
 }
 
@@ -405,9 +409,12 @@ int train_launches(bp_net* net, const BatchInput& in, const float* targets, int6
     if (b.act) b.act += (size_t)p0 * b.n_active;
     const float* Tb = targets + (size_t)p0 * net->n[net->L];
     if (use_small(net, b)) {
-      rc = run_small(net, b, rows, Tb, net->sse_part + used, lr, mom);
+      const bool last = p0 + batch >= n;
+      const size_t total = used + (size_t)sse_blocks(net, b, rows);
+      rc = run_small(net, b, rows, Tb, net->sse_part + used, lr, mom, last ? (int)total : -1);
       if (rc) return rc;
-      used += (size_t)sse_blocks(net, b, rows);
+      used = total;
+      if (last) return BP_OK;   // the error sum went with the last update
       continue;
     }
     rc = run_forward(net, b, rows, Tb, net->sse_part + used, nullptr, 0, net->act.data());

@@ -282,8 +282,16 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
                                                            const float* __restrict__ D2, int ldd2, float* W0,
                                                            float* V0, int ldw0, int n0, int H, float* W1, float* V1,
                                                            int ldw1, int O, int nT, int ch, float lr, float mom,
-                                                           float limit, unsigned long long* faults) {
+                                                           float limit, unsigned long long* faults,
+                                                           const double* __restrict__ sse_part, int n_sse,
+                                                           double* sse_out) {
   extern __shared__ f32x4 stage[];
+  // The last update of a call has one more block, which sums the call's error
+  // partials (all written by the forward/backward kernels before this launch).
+  if (sse_out && (int)blockIdx.x == (int)gridDim.x - 1) {
+    block_sum_partials<kTU>(sse_part, n_sse, sse_out, reinterpret_cast<double*>(stage));
+    return;
+  }
   __shared__ float part[kWU][64];
   __shared__ float tile_sum[256];
   __shared__ int list[kTU];
@@ -579,18 +587,23 @@ hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int row
 
 hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int rows, const float* A1q, const float* D1,
                         int ldd1, const float* D2, int ldd2, float* W0, float* V0, int ldw0, int n0, int H, float* W1,
-                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults) {
+                        float* V1, int ldw1, int O, float lr, float mom, float limit, unsigned long long* faults,
+                        const double* sse_part, int n_sse, double* sse_out) {
   if (rows <= 0) return hipSuccess;
   const int nT = (H + 1 + 3) / 4;
   const int nS = (H + 31) / 32;
   const int ch = small_update_chunk(O), o4 = small_op(O) / 4;
   // tile chunks: ch (o4 + 1) + 64 float4; bias-row chunks: 512 rows of 8 float4
+  // (at least kTU doubles for the error sum)
   const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1) + 64, (size_t)512 * 8);
+  const int blocks = nT + n0 + nS + (sse_out ? 1 : 0);
   if (limit > 0.f)
-    return launch_kernel(small_update_kernel<true>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1q, rows, D1,
-                         ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
-  return launch_kernel(small_update_kernel<false>, nT + n0 + nS, kTU, lds, s, act, n_active, rows, A1q, rows, D1,
-                       ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults);
+    return launch_kernel(small_update_kernel<true>, blocks, kTU, lds, s, act, n_active, rows, A1q, rows, D1, ldd1, D2,
+                         ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults, sse_part, n_sse,
+                         sse_out);
+  return launch_kernel(small_update_kernel<false>, blocks, kTU, lds, s, act, n_active, rows, A1q, rows, D1, ldd1, D2,
+                       ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults, sse_part, n_sse,
+                       sse_out);
 }
 
 }  // namespace bpk
