@@ -179,13 +179,16 @@ def test_sequence_arguments_are_checked(dev):
 # Context copying hidden layer 1 in order: the first product builds the step's
 # input rows itself.  Cases: external inputs not a multiple of 4 wide (scalar
 # loads), one step per window (the source rows are the ones the step writes:
-# those steps build the rows first), no external input, and a context of the
-# first 24 of 40 hidden units.
+# those steps build the rows first), no external input, a context of the
+# first 24 of 40 hidden units, and a net too large for that path (2000
+# streams x 300 hidden units: assembled rows and tiled products).
 BUILT_INPUT_SPECS = [
     wl.SeqSpec("elman-built-13+40", 13, (40,), 9, 40, 70, 23, 4, 3, 9, 0.01, 0.9, 2, 31),
     wl.SeqSpec("elman-built-1-step", 16, (40,), 9, 40, 70, 11, 1, 3, 9, 0.01, 0.9, 2, 32),
     wl.SeqSpec("elman-built-0+40", 0, (40,), 9, 40, 70, 17, 4, 3, 9, 0.01, 0.9, 2, 33),
     wl.SeqSpec("elman-built-8+24of40", 8, (40, 16), 9, 24, 70, 17, 5, 3, 9, 0.01, 0.9, 2, 34),
+    # too many output tiles for the skinny kernel: input assembly, then the tiled products
+    wl.SeqSpec("elman-tiled-10+300", 10, (300,), 7, 300, 2000, 6, 3, 2, 5, 0.001, 0.9, 1, 35),
 ]
 
 
