@@ -109,7 +109,11 @@ def _half_sse(net, w, x, t):
     return 0.5 * np.sum((t.astype(np.float64) - y) ** 2)
 
 
-@pytest.mark.parametrize("sizes,n", [((3, 4, 2), 3), ((5, 3, 4, 2), 3), ((4, 1), 5), ((2, 7, 1), 4)])
+# Nets of equal widths are included because there a mix-up of layers or a
+# transposed weight block still has the right shape, so only the values can
+# show it.
+@pytest.mark.parametrize("sizes,n", [((3, 4, 2), 3), ((5, 3, 4, 2), 3), ((4, 1), 5), ((2, 7, 1), 4), ((3, 3, 3), 3),
+                                     ((4, 4, 4, 4), 2)])
 def test_summed_change_is_negative_gradient_central_differences(sizes, n):
     x, t, w = _rand_case(sizes, n, seed=sum(sizes) + n)
     net = _net(sizes, w)
