@@ -78,12 +78,12 @@ __host__ __device__ __forceinline__ int small_op(int O) { return (O + 31) / 32 *
 //   hs   P x HP       hidden activations (units H .. HP-1 zero)
 //   d2s  P x OP       output deltas (outputs O .. OP-1 zero)
 //   ts   P x O + 64   targets
-//   idx  P x n_active + 64  active input indices (int)
-// (the 64 extra entries of b1s, ts and idx take the round-1 stores of the
-// lanes past the end, one entry per lane)
+// (the 64 extra entries of b1s and ts take the round-1 stores of the lanes
+// past the end, one entry per lane)
 __host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H, int O, int n_active) {
   const int Hp = small_hp(H), Op = small_op(O);
-  return (size_t)Hp * (Op + 4) + Op + 64 + (size_t)P * (Hp + Op) + (size_t)P * O + 64 + (size_t)P * n_active + 64;
+  (void)n_active;
+  return (size_t)Hp * (Op + 4) + Op + 64 + (size_t)P * (Hp + Op) + (size_t)P * O + 64;
 }
 
 // 1024 threads (16 waves, four per SIMD) per block of P patterns.  With so
@@ -92,8 +92,9 @@ __host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H,
 // the padded extents HP = small_hp(H) and OP = small_op(O) are template
 // parameters: every LDS read of the sums below uses a constant offset from
 // one base address, and the staging loop has a fixed trip count.
-//   round 1   indices, targets, the bias row and W1 (HP OP / 1024 elements
-//             per thread): all loads issued before any is waited on;
+//   round 1   each gather item's active indices, then targets, the bias
+//             row and W1 (HP OP / 1024 elements per thread), then the
+//             gather's W0 rows as soon as their indices arrive;
 //   gather    one (pattern, hidden unit) pair per thread: bias + the active
 //             rows of W0, in index order -> sigma;
 //   output    each output (p, c) summed by 16 adjacent lanes, lane k over
@@ -124,7 +125,6 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   float* hs = b1s + OP + 64;                                 // P x HP
   float* d2s = hs + P * HP;                                  // P x OP
   float* ts = d2s + P * OP;                                  // P x O + 64
-  int* idx = reinterpret_cast<int*>(ts + P * O + 64);        // P x n_active + 64
   __shared__ float red[kT / 64];
 
   const int tid = threadIdx.x;
@@ -132,49 +132,75 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   const int np = min(P, rows - p0);
   const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
-  // round 1 (np * n_active <= 256, np * O <= 512 and P * OP <= 512 <= kT by
-  // the path's limits).  Every load reads a clamped, valid address and is
-  // stored to LDS unconditionally (the value selected; lanes past the end
-  // store to a spare entry of their own), so that no load is sunk behind a
-  // branch and all are in flight together.  (Rows of act and of T are
-  // contiguous.)
-  {
-    const int ni = np * n_active, nt = np * O;
-    const int iv = act[(size_t)p0 * n_active + min(tid, ni - 1)];
-    const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
-    const float bv = W1[(size_t)H * ldw1 + min(tid, O - 1)];
-    const int c = tid & (OP - 1), jt = tid / OP;
-    const float* wsrc = W1 + min(c, O - 1);
-    float v[NW];
+  // Loads in three groups, all in flight before the first is waited on:
+  // each gather item's active indices, then the staging round, then the
+  // gather's W0 rows, issued as soon as their indices arrive.  The thread of
+  // gather item t = (pattern p, hidden unit j) reads its pattern's indices
+  // straight from global memory (they depend on nothing staged here), so the
+  // gather's loads overlap the staging round instead of following it.  Items
+  // past the block's patterns read clamped, valid addresses and store nothing.
+  constexpr int NG = (P * HP + kT - 1) / kT;                 // gather items per thread
+  int iv[NG][8];
 #pragma unroll
-    for (int u = 0; u < NW; ++u) v[u] = wsrc[(size_t)min(jt + u * RPP, H - 1) * ldw1];
+  for (int g = 0; g < NG; ++g) {
+    const int p = min((tid + g * kT) >> LHP, np - 1);
+    const int32_t* ip = act + (size_t)(p0 + p) * n_active;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) iv[g][u] = ip[min(u, n_active - 1)];
+  }
+  // Staging round (np * O <= 512 and P * OP <= 512 <= kT by the path's
+  // limits).  Every load reads a clamped, valid address and is stored to LDS
+  // unconditionally (the value selected; lanes past the end store to a spare
+  // entry of their own), so that no load is sunk behind a branch.  (Rows of T
+  // are contiguous.)
+  const int nt = np * O;
+  const float t0 = T[(size_t)p0 * O + min(tid, nt - 1)];
+  const float bv = W1[(size_t)H * ldw1 + min(tid, O - 1)];
+  const int c1 = tid & (OP - 1), jt = tid / OP;
+  float v1[NW];
+  {
+    const float* wsrc = W1 + min(c1, O - 1);
+#pragma unroll
+    for (int u = 0; u < NW; ++u) v1[u] = wsrc[(size_t)min(jt + u * RPP, H - 1) * ldw1];
+  }
+  // keep the W0 loads behind the staging loads: waiting for an index must not
+  // hold back the staging round
+  __builtin_amdgcn_sched_barrier(0);
+  float gv[NG][8], gb[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int jc = min((tid + g * kT) & (HP - 1), H - 1);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) gv[g][u] = W0[(size_t)iv[g][u] * ldw0 + jc];
+    gb[g] = W0[(size_t)n0 * ldw0 + jc];
+  }
+  {
 #pragma unroll
     for (int u = 0; u < NW; ++u) {
       const int j = jt + u * RPP;
-      w1s[j * S1 + c] = (j < H && c < O) ? v[u] : 0.f;
+      w1s[j * S1 + c1] = (j < H && c1 < O) ? v1[u] : 0.f;
     }
     const int spare = tid & 63;
     b1s[tid < OP ? tid : OP + spare] = tid < O ? bv : 0.f;
-    idx[tid < ni ? tid : P * n_active + spare] = iv;
     ts[tid < nt ? tid : P * O + spare] = t0;
     if (tid < P * OP && (tid & (OP - 1)) >= O) d2s[tid] = 0.f;
   }
-  __syncthreads();
   // gather: net = bias + the active rows of W0 (in index order); units
   // H .. HP-1 get 0
-  for (int t = tid; t < np * HP; t += kT) {
-    const int p = t >> LHP, j = t & (HP - 1), jc = min(j, H - 1);
-    const int* ip = idx + p * n_active;
-    float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = W0[(size_t)ip[min(u, n_active - 1)] * ldw0 + jc];
-    float net = W0[(size_t)n0 * ldw0 + jc];
+  for (int g = 0; g < NG; ++g) {
+    const int t = tid + g * kT;
+    if (t < np * HP) {
+      const int p = t >> LHP, j = t & (HP - 1), jc = min(j, H - 1);
+      float net = gb[g];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (u < n_active) net += v[u];
-    for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + jc];
-    const float h = TAB ? logistic_table(net, tab) : logistic(net);
-    hs[t] = j < H ? h : 0.f;
+      for (int u = 0; u < 8; ++u)
+        if (u < n_active) net += gv[g][u];
+      const int32_t* ip = act + (size_t)(p0 + p) * n_active;
+      for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + jc];
+      const float h = TAB ? logistic_table(net, tab) : logistic(net);
+      hs[t] = j < H ? h : 0.f;
+    }
   }
   __syncthreads();
   // Output layer, output deltas and squared error.
