@@ -132,7 +132,10 @@ int hip_fail(bp_net* net, hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail((net), e_, #expr); \
   } while (0)
 
-int round4(int v) { return (v + 3) / 4 * 4; }
+// Weight, activation and delta rows are padded to 32 floats, one 128-byte
+// cache line: a row that one block writes then shares no line with a row
+// that a block on another XCD writes (each XCD has its own L2).
+int row_pad(int v) { return (v + 31) / 32 * 32; }
 
 hipEvent_t take_event(bp_net* net) {
   if (!net->ev_pool.empty()) {
@@ -773,9 +776,9 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
   net->woff.resize(net->L);
   net->foff.resize(net->L);
   net->lda.resize(net->L + 1);
-  for (int l = 0; l <= net->L; ++l) net->lda[l] = round4(net->n[l]);
+  for (int l = 0; l <= net->L; ++l) net->lda[l] = row_pad(net->n[l]);
   for (int l = 0; l < net->L; ++l) {
-    net->ldw[l] = round4(net->n[l + 1]);
+    net->ldw[l] = row_pad(net->n[l + 1]);
     net->woff[l] = net->wtotal;
     net->foff[l] = net->nweights;
     net->wtotal += (int64_t)(net->n[l] + 1) * net->ldw[l];

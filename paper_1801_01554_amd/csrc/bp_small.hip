@@ -128,7 +128,11 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   __shared__ float red[kT / 64];
 
   const int tid = threadIdx.x;
-  const int p0 = blockIdx.x * P;
+  // blocks of one XCD (hardware block b runs on XCD b % 8) take a contiguous
+  // range of patterns
+  const int nbk = gridDim.x, xcd = blockIdx.x & 7, qb = nbk >> 3, rb = nbk & 7;
+  const int lb = xcd * qb + min(xcd, rb) + (blockIdx.x >> 3);
+  const int p0 = lb * P;
   const int np = min(P, rows - p0);
   const float inv_O = 1.0f / (float)O, inv_H = 1.0f / (float)H;
 
@@ -271,7 +275,7 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   if (tid == 0) {
     double s = 0.0;
     for (int w = 0; w < kT / 64; ++w) s += (double)red[w];
-    sse_part[blockIdx.x] = s;
+    sse_part[lb] = s;
   }
 }
 
