@@ -290,11 +290,13 @@ __host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 
 // LDS by one round of coalesced loads, every load stored unconditionally so
 // that none is sunk behind a branch.
 // Blocks [0, nT): rows j0 .. j0+3 of W1 (j0 = 4 b; row H is the bias row,
-//   activation 1), all O columns: G[j][c] = sum_p A1[p][j] D2[p][c].  Waves
-//   0-7 compute: lane (sub, g) holds the 4 x 4 tile of rows j0 .. j0+3 and
-//   columns 4 sub .. 4 sub + 3 over the patterns g, g + ng, g + 2 ng, ... in
-//   order (ng = 512 / (Op / 4) lane groups); the group sums are then added
-//   through LDS in a fixed tree.
+//   activation 1), all O columns: G[j][c] = sum_p A1[p][j] D2[p][c].  The
+//   first NCW threads compute: lane (sub, g) holds the 4 x 4 tile of rows
+//   j0 .. j0+3 and columns 4 sub .. 4 sub + 3 over the patterns g, g + ng,
+//   g + 2 ng, ... in order (ng = NCW / (Op / 4) lane groups); the group sums
+//   are then added through LDS in a fixed tree.  NCW (128, 256 or 512) grows
+//   with the batch: a small batch leaves most lanes without patterns, and
+//   fewer group sums are cheaper to combine.
 // Blocks [nT, nT + n0): row r of W0: the delta rows of the patterns whose
 //   active list holds r, in pattern order (ballot compaction of 1024
 //   patterns at a time); with ns = 1, 2 or 4 strips of 64 columns covering
@@ -305,7 +307,16 @@ __host__ __device__ __forceinline__ int small_update_chunk(int O) { return 4096 
 //   slices of each chunk in pattern order, the 32 slice sums combined in
 //   slice order.
 // CHECK: the range check of the summed changes (limit > 0).
-template <bool CHECK>
+// Sum of N values in a fixed pairwise tree.
+template <int N>
+__device__ __forceinline__ float tree_sum(const float* v) {
+  if constexpr (N == 1)
+    return v[0];
+  else
+    return tree_sum<N / 2>(v) + tree_sum<N / 2>(v + N / 2);
+}
+
+template <bool CHECK, int NCW>
 __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __restrict__ act, int n_active, int rows,
                                                            const float* __restrict__ A1q, int ldq,
                                                            const float* __restrict__ D1, int ldd1,
@@ -368,7 +379,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     f32x4* a1s = stage + ch * o4;                    // [ch + 64]: activations of rows j0 .. j0+3
     const f32x4* a1g = reinterpret_cast<const f32x4*>(A1q) + (size_t)min(b, (H - 1) >> 2) * ldq;
     const f32x4* d2g = reinterpret_cast<const f32x4*>(D2);
-    const int sub = tid & (o4 - 1), grp = tid >> lo4, ng = 512 >> lo4;
+    const int sub = tid & (o4 - 1), grp = tid >> lo4, ng = NCW >> lo4;
     float acc[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
@@ -401,7 +412,7 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
         a1s[tid < ch ? tid : ch + lane] = av;
       }
       __syncthreads();
-      if (tid < 512) {
+      if (tid < NCW) {
         for (int p = grp; p < cn; p += 4 * ng) {
           f32x4 a[4], d[4];
 #pragma unroll
@@ -426,10 +437,10 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
     // accs[grp * S + i * Op + 4 sub + q] (acc[4 i + q]; row stride S = 16 o4
     // + 8 floats keeps both the writes and the strided reads below free of
     // bank conflicts).  Element el = i * Op + 4 sub + q is summed by
-    // tpe = 1024 / (16 o4) adjacent threads, thread s over the 8 groups s,
-    // s + tpe, ..., the partial sums combined by group_sum.
+    // tpe = 1024 / (16 o4) adjacent threads, thread s over the NCW / 64
+    // groups s, s + tpe, ..., the partial sums combined by group_sum.
     const int S4 = 4 * o4 + 2;                           // row stride in float4
-    if (tid < 512) {
+    if (tid < NCW) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         stage[grp * S4 + i * o4 + sub] = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
@@ -439,10 +450,11 @@ __global__ __launch_bounds__(kTU) void small_update_kernel(const int32_t* __rest
       const int lt = 6 - lo4, tpe = 1 << lt;             // 8 (o4 = 8) or 4 (o4 = 16)
       const int el = tid >> lt, sl = tid & (tpe - 1);
       const float* src = reinterpret_cast<const float*>(stage) + el;
-      float v[8];
+      constexpr int GPT = NCW / 64;                      // ng = GPT tpe groups
+      float v[GPT];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = src[(sl + tpe * u) * (4 * S4)];   // ng = 8 tpe groups
-      float x = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7])));
+      for (int u = 0; u < GPT; ++u) v[u] = src[(sl + tpe * u) * (4 * S4)];
+      float x = tree_sum<GPT>(v);
       x = group_sum(x, lt);
       if (sl == 0) tile_sum[el] = x;
     }
@@ -627,13 +639,25 @@ hipError_t small_update(hipStream_t s, const int32_t* act, int n_active, int row
   // (at least kTU doubles for the error sum)
   const size_t lds = 16 * std::max((size_t)ch * (size_t)(o4 + 1) + 64, (size_t)512 * 8);
   const int blocks = nT + n0 + nS + (sse_out ? 1 : 0);
-  if (limit > 0.f)
-    return launch_kernel(small_update_kernel<true>, blocks, kTU, lds, s, act, n_active, rows, A1q, rows, D1, ldd1, D2,
-                         ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults, sse_part, n_sse,
-                         sse_out);
-  return launch_kernel(small_update_kernel<false>, blocks, kTU, lds, s, act, n_active, rows, A1q, rows, D1, ldd1, D2,
-                       ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults, sse_part, n_sse,
-                       sse_out);
+  // W1-tile compute width by batch (measured at 16 rows: 512 lanes 7.62, 256
+  // lanes 7.41, 128 lanes 7.39 us per update; at 512 rows 512 lanes are best)
+  const int ncw = rows <= 64 ? 128 : (rows <= 256 ? 256 : 512);
+#define BP_UPD(CHK, NCWV)                                                                                          \
+  if (ncw == NCWV)                                                                                                 \
+    return launch_kernel(small_update_kernel<CHK, NCWV>, blocks, kTU, lds, s, act, n_active, rows, A1q, rows, D1, \
+                         ldd1, D2, ldd2, W0, V0, ldw0, n0, H, W1, V1, ldw1, O, nT, ch, lr, mom, limit, faults,      \
+                         sse_part, n_sse, sse_out);
+  if (limit > 0.f) {
+    BP_UPD(true, 128)
+    BP_UPD(true, 256)
+    BP_UPD(true, 512)
+  } else {
+    BP_UPD(false, 128)
+    BP_UPD(false, 256)
+    BP_UPD(false, 512)
+  }
+#undef BP_UPD
+  return hipErrorInvalidValue;
 }
 
 }  // namespace bpk
