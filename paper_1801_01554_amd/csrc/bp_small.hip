@@ -80,9 +80,8 @@ __host__ __device__ __forceinline__ int small_op(int O) { return (O + 31) / 32 *
 //   ts   P x O + 64   targets
 // (the 64 extra entries of b1s and ts take the round-1 stores of the lanes
 // past the end, one entry per lane)
-__host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H, int O, int n_active) {
+__host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H, int O) {
   const int Hp = small_hp(H), Op = small_op(O);
-  (void)n_active;
   return (size_t)Hp * (Op + 4) + Op + 64 + (size_t)P * (Hp + Op) + (size_t)P * O + 64;
 }
 
@@ -618,7 +617,7 @@ hipError_t small_fwdbwd(hipStream_t s, const int32_t* act, int n_active, int row
                         float* D2, int ldd2, double* sse_part, const float* tab) {
   if (rows <= 0) return hipSuccess;
   const int P = patterns_per_block(rows);
-  const size_t lds = sizeof(float) * small_fwdbwd_lds_floats(P, H, O, n_active);
+  const size_t lds = sizeof(float) * small_fwdbwd_lds_floats(P, H, O);
   const int nb = small_fwdbwd_blocks(rows);
   if (tab)
     return launch_fwdbwd<true>(s, P, nb, lds, act, n_active, rows, W0, ldw0, n0, H, W1, ldw1, O, T, A1q, D1, ldd1,
