@@ -4,16 +4,19 @@
 
 A step is one pooled update: forward pass, output and hidden deltas, summed
 change and learning-rate/momentum update over one batch (all on the GPU,
-inputs resident in HBM).  The primary workload is the NETtalk-shaped
-203-120-26 net with one-hot 7 x 29 window inputs, batch 512, 20,000
-patterns; its steps follow the epoch structure (40 updates per epoch, the
-last of 32 patterns), one library call per epoch: after two untimed epochs
-the library replays each epoch call from the HIP graph it captured (the
-same kernels with less launch overhead).  The wide (1024-4096-1024, batch 4096) and deep
-(512-2048-2048-2048-64, batch 8192) dense nets run one full epoch each and
-are reported under "secondary", with the Elman net (64 external inputs +
-256 context units, 256 hidden, 64 outputs; 1024 parallel sequence streams,
-an update every 8 steps) and the primary workload with the table sigmoid and
+inputs resident in HBM).  The headline workload is the deep dense net
+512-2048-2048-2048-64 (batch 8192, 524,288 N(0,1) patterns, one epoch = 64
+updates), the largest of the five workloads and the one on which the fp32
+MFMA fraction is measured.  K updates are timed as one library call over
+K x 8192 patterns; before it, W untimed updates warm the clocks, and two
+calls identical to the timed one let the library capture its replay graph,
+so that the timed call replays it whatever W is.
+
+Under "secondary": the wide dense net 1024-4096-1024 (one epoch), the
+NETtalk-shaped one-hot nets 203-80-26 (one update), 203-120-26 at batch 512
+(10 epochs) and at batch 16 (2 epochs), the Elman net (64 external inputs +
+256 context units, 256 hidden, 64 outputs; 1024 sequence streams, an update
+every 8 steps), and the batch-512 NETtalk net with the table sigmoid and
 with the range check of the summed changes switched on.
 
 value = connections x patterns presented / wall time (the paper's
@@ -21,11 +24,11 @@ definition, section 7.1: bias connections included, update frequency and
 cheaper input connections not accounted for).
 
 Per-kernel device times come from a second pass over the same steps in which
-the library brackets every launch with HIP events on its stream (direct
-launches, no graph); the
-dominant kernel's algorithmic work per launch divided by its average
-duration gives the roofline entry.  The oracle (CPU, test infrastructure) is
-timed on a bounded sample for the CPU baseline.
+the library brackets every launch with HIP events on the stream it runs on
+(direct launches, no graph); the dominant kernel's algorithmic work per
+launch divided by its average duration gives the roofline entry.  The oracle
+(CPU, test infrastructure) is timed on a bounded sample for the CPU
+baseline.
 """
 from __future__ import annotations
 
@@ -43,8 +46,9 @@ METRIC = "connection-updates/sec (fwd+bwd+update) and % fp32 MFMA peak, 1 MI355X
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix peak, flop/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E, bytes/s
 PAPER_GF11_CPS = 9.01e8     # section 6.3, Table 1: 356 processors, tree summation
-PRIMARY = "nettalk-120-b512"
-SECONDARY = ("wide-1024-4096-1024", "deep-512-2048x3-64")
+PRIMARY = "deep-512-2048x3-64"
+SECONDARY = ("wide-1024-4096-1024", "nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16")
+VARIANT_WORKLOAD = "nettalk-120-b512"
 SECONDARY_SEQ = ("elman-64+256-256-64",)
 GEMM_KINDS = ("forward", "output", "backward", "change", "seq_pair")
 KERNEL_NAMES = {
@@ -78,11 +82,12 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
     L = len(sizes) - 1
     R = float(rows)
     if onehot and L == 2 and sizes[1] <= SMALL_MAX_HIDDEN and sizes[2] <= SMALL_MAX_OUT and n_active <= SMALL_MAX_ACTIVE:
+        # The algorithmic bytes of one update are 4 (n_active + n_L) per pattern (indices and
+        # targets, read by the forward/backward launch) and 16 per weight (W and V read and
+        # written, by the update launch); intermediates (activations, deltas) are not counted.
         n0, H, O = sizes
-        add("fused_fb", R * (H * (n_active + 1) + 4 * H * O),
-            4 * (R * n_active + (n0 + 1) * H + (H + 1) * O + R * O + 2 * R * H + R * O))
-        add("fused_update", R * (2 * (H + 1) * O + H * (n_active + 1)),
-            4 * (R * n_active + 2 * R * H + R * O) + 16 * ((n0 + 1) * H + (H + 1) * O))
+        add("fused_fb", R * (H * (n_active + 1) + 4 * H * O), 4.0 * R * (n_active + O))
+        add("fused_update", R * (2 * (H + 1) * O + H * (n_active + 1)), 16.0 * ((n0 + 1) * H + (H + 1) * O))
         return w
     fwd, bwd = "fwd" in parts, "bwd" in parts
     for l in range(L):
@@ -208,7 +213,12 @@ def step_rows(spec, calls):
 
 
 def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None):
-    """Times `steps` pooled updates of a named workload (variant: "table sigmoid" or "range check")."""
+    """Times `steps` pooled updates of a named workload (variant: "table sigmoid" or "range check").
+
+    The timed updates run as the calls of schedule(spec, steps) (one call per epoch, in epoch
+    order).  Before them: `warmup` untimed updates (clock warm-up), then the same calls twice,
+    so that the library has captured them into its replay graph (it captures the second of two
+    identical calls) and the timed calls replay it, whatever `warmup` is."""
     spec = wl.SPECS[name]
     t0 = time.time()
     w = wl.make(name)
@@ -237,13 +247,17 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None)
     if warmup:
         net.set_weights(w.weights)
         run(schedule(spec, warmup))
+    for _ in range(2):                    # the second identical call captures the replay graph
+        net.set_weights(w.weights)
+        run(calls)
     net.set_weights(w.weights)            # timed run starts from the workload's initial state
     torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()  # the library's stream (bp.Net enqueues on torch's current stream)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
-    ev0.record()
+    ev0.record(stream)
     run(calls)
-    ev1.record()
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     secs = ev0.elapsed_time(ev1) / 1e3
@@ -263,9 +277,10 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None)
 
     W = metrics.num_weights(w.sizes)
     cps = W * patterns / secs
-    flops_step = sum(metrics.dense_flops_per_pattern(w.sizes, r) * r for r in step_rows(spec, calls))
+    rows = step_rows(spec, calls)
+    flops_step = sum(metrics.dense_flops_per_pattern(w.sizes, r) * r for r in rows)
     work = {}
-    for r in step_rows(spec, calls):
+    for r in rows:
         for k, (f, b) in kind_work(w.sizes, r, w.active is not None, 7, change_splits).items():
             f0, b0 = work.get(k, (0.0, 0.0))
             work[k] = (f0 + f, b0 + b)
@@ -278,6 +293,13 @@ def run_workload(name, steps, warmup, torch, bp, wl, metrics, log, variant=None)
         "us_per_update": secs * 1e6 / steps, "roofline": roof, "kernels": kernels,
         "kernel_time_ms": sum(v["total_ms"] for v in kernels.values()),
     }
+    if w.active is not None:
+        # the whole update against HBM: 16 B per weight (W, V read and written) + 4 (n_active + n_L) B
+        # per pattern (indices, targets), over the measured time per update
+        upd_bytes = sum(metrics.onehot_bytes_per_update(w.sizes) +
+                        r * metrics.onehot_bytes_per_pattern(w.sizes, w.active.shape[1]) for r in rows)
+        res["update_hbm"] = {"algorithmic_bytes_per_update": upd_bytes / steps,
+                             "achieved_gbps": upd_bytes / secs / 1e9, "frac": upd_bytes / secs / PEAK_HBM}
     if variant:
         res["variant"] = variant
     return res, w
@@ -494,43 +516,35 @@ def counters_to_traffic(workload, fetch_csv, write_csv, calib_fetch_csv, calib_w
     print(json.dumps(d["workloads"][workload], indent=1))
 
 
-def cpu_baseline(w, budget_s, log):
-    """The oracle (double storage) on the host cores, whole epochs of the workload until the budget is spent."""
+def cpu_baseline(w, budget_s, log, max_updates=None):
+    """The oracle (double storage) on the host cores: the workload's updates in order (whole
+    epochs of batches, momentum carried) until `budget_s` seconds are spent, at least one update,
+    at most the workload's own updates (or `max_updates`)."""
     import oracle
     from paper_1801_01554_amd import metrics
     spec = w.spec
     o = oracle.OracleNet(w.sizes, 64)
     o.set_weights(w.weights.astype("float64"))
-    kw = {"active": w.active} if w.active is not None else {"x": w.inputs}
+    per_epoch = -(-w.n_patterns // spec.batch)
+    total = per_epoch * spec.epochs if max_updates is None else min(max_updates, per_epoch * spec.epochs)
     t0 = time.perf_counter()
-    epochs = 0
-    while epochs < spec.epochs:
-        o.train_epoch(w.targets, spec.batch, w.lr, w.momentum, **kw)
-        epochs += 1
+    done, pats = 0, 0
+    while done < total:
+        b0 = (done % per_epoch) * spec.batch
+        n = min(spec.batch, w.n_patterns - b0)
+        kw = {"active": w.active[b0:b0 + n]} if w.active is not None else {"x": w.inputs[b0:b0 + n]}
+        o.train_epoch(w.targets[b0:b0 + n], spec.batch, w.lr, w.momentum, **kw)
+        done += 1
+        pats += n
         if time.perf_counter() - t0 >= budget_s:
             break
     secs = time.perf_counter() - t0
-    pats = epochs * w.n_patterns
     v = metrics.num_weights(w.sizes) * pats / secs
-    log(f"[cpu] oracle {epochs} epoch(s), {pats} patterns in {secs:.2f}s on {oracle.get_threads()} threads")
+    log(f"[cpu] oracle {done} update(s) of {spec.name}, {pats} patterns in {secs:.2f}s on {oracle.get_threads()} "
+        f"threads")
     return {"value": v, "unit": "connections/s", "cores": oracle.get_threads(), "kind": "oracle",
-            "sample": f"{epochs} of {spec.epochs} epochs of {w.spec.name} ({pats} patterns), {secs:.2f} s"}
-
-
-def cpu_sample_batch(w, log):
-    """The oracle on the first batch only (one pooled update), for the large dense nets."""
-    import oracle
-    from paper_1801_01554_amd import metrics
-    spec = w.spec
-    o = oracle.OracleNet(w.sizes, 64)
-    o.set_weights(w.weights.astype("float64"))
-    n = spec.batch
-    t0 = time.perf_counter()
-    o.train_epoch(w.targets[:n], spec.batch, w.lr, w.momentum, x=w.inputs[:n])
-    secs = time.perf_counter() - t0
-    log(f"[cpu] oracle 1 update of {w.spec.name} in {secs:.2f}s")
-    return {"value": metrics.num_weights(w.sizes) * n / secs, "unit": "connections/s",
-            "cores": oracle.get_threads(), "kind": "oracle", "sample": f"first update ({n} patterns), {secs:.2f} s"}
+            "sample": f"the first {done} of {per_epoch * spec.epochs} updates of {spec.name} in order ({pats} "
+                      f"patterns, batch {spec.batch}), {secs:.2f} s"}
 
 
 def main():
@@ -538,10 +552,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="pooled updates timed (default: the whole workload)")
     ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed updates first (default: two epochs, so that the library has captured the "
-                         "repeated epoch call into its replay graph before timing starts)")
+                    help="untimed updates first, to warm the clocks (default 4); two untimed calls identical to "
+                         "the timed one always follow, so that the library replays its captured graph in the "
+                         "timed call")
     ap.add_argument("--workload", default=PRIMARY)
-    ap.add_argument("--no-secondary", action="store_true", help="skip the wide and deep dense nets")
+    ap.add_argument("--no-secondary", action="store_true", help="time the headline workload only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for the baseline")
     ap.add_argument("--copy-calibration", action="store_true", help="only copy 1 GiB four times (counter scale)")
@@ -589,8 +604,11 @@ def main():
     spec = wl.SPECS[args.workload]
     per_epoch = -(-spec.n_patterns // spec.batch)
     steps = args.steps if args.steps is not None else per_epoch * spec.epochs
-    warmup = args.warmup if args.warmup is not None else 2 * per_epoch
+    warmup = args.warmup if args.warmup is not None else 4
     prim, w = run_workload(args.workload, steps, warmup, torch, bp, wl, metrics, log)
+    cpu = cpu_baseline(w, args.cpu_budget, log) if not args.no_cpu else None
+    del w
+    torch.cuda.empty_cache()
 
     secondary = []
     if not args.no_secondary:
@@ -601,7 +619,7 @@ def main():
             pe = -(-s2.n_patterns // s2.batch)
             r, w2 = run_workload(name, pe * s2.epochs, 4, torch, bp, wl, metrics, log)
             if not args.no_cpu:
-                r["cpu_baseline"] = cpu_sample_batch(w2, log)
+                r["cpu_baseline"] = cpu_baseline(w2, min(args.cpu_budget, 5.0), log)
             secondary.append(r)
             del w2
             torch.cuda.empty_cache()
@@ -610,8 +628,10 @@ def main():
             secondary.append(r)
             del w2
             torch.cuda.empty_cache()
+        sv = wl.SPECS[VARIANT_WORKLOAD]
         for variant in ("table sigmoid", "range check"):
-            r, _ = run_workload(args.workload, steps, warmup, torch, bp, wl, metrics, log, variant=variant)
+            r, _ = run_workload(VARIANT_WORKLOAD, -(-sv.n_patterns // sv.batch) * sv.epochs, 4, torch, bp, wl,
+                                metrics, log, variant=variant)
             secondary.append(r)
 
     line = {
@@ -622,13 +642,15 @@ def main():
                    "patterns_per_epoch": spec.n_patterns, "patterns_timed": prim["patterns"],
                    "inputs": "one-hot 7x29 window" if spec.onehot else spec.input_kind,
                    "lr": spec.lr, "momentum": spec.momentum, "parallelism": "single GPU"},
-        "mfma_peak_frac": prim["mfma_peak_frac"], "us_per_update": prim["us_per_update"],
-        "roofline": prim["roofline"], "kernels": prim["kernels"],
+        "mfma_peak_frac": prim["mfma_peak_frac"], "gemm_mfma_frac": prim["gemm_mfma_frac"],
+        "us_per_update": prim["us_per_update"], "roofline": prim["roofline"], "kernels": prim["kernels"],
         "context": {"paper_gf11_cps": PAPER_GF11_CPS, "note": "GF11, 356 processors, NETtalk 203-60-26 (section 6.3)"},
         "secondary": secondary,
     }
-    if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, log)
+    if prim.get("update_hbm"):
+        line["update_hbm"] = prim["update_hbm"]
+    if cpu:
+        line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
 
 

@@ -55,9 +55,15 @@ enum {
   BP_EDEVICE = -3   /* HIP runtime error */
 };
 
-/* Creates a net with layer sizes layer_sizes[0 .. n_layers-1] (each >= 1,
- * n_layers >= 2) on the current HIP device.  Weights and momentum start at
- * zero.  *out receives the handle (NULL on failure). */
+/* Creates a net with layer sizes layer_sizes[0 .. n_layers-1] (each >= 1 and
+ * <= 2^24, n_layers >= 2; host array, read during the call) on the current
+ * HIP device: a fully connected feed-forward net given by its topology, as
+ * the paper's simulator builds its code from a topology file (section 2),
+ * each non-input layer also fed by the true unit (section 6.3).  Weights and
+ * momentum start at zero.  *out receives the handle (NULL on failure); the
+ * caller releases it with bp_destroy.  BP_EINVAL for a NULL out or
+ * layer_sizes, or sizes out of range; BP_ENOMEM / BP_EDEVICE if the device
+ * allocation fails (nothing is left allocated). */
 int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out);
 
 /* Frees the net and its device memory after its stream has drained.  NULL is a no-op. */
@@ -67,27 +73,35 @@ void bp_destroy(bp_net* net);
  * all later work of this net is enqueued on.  NULL selects the null stream. */
 int bp_set_stream(bp_net* net, void* hip_stream);
 
-/* Number of weights = connections, bias rows included (section 6.3, section 7.1).
- * Returns -1 for a NULL net. */
+/* Number of weights = connections, bias rows included: the paper's
+ * connection count (section 6.3) that its throughput unit counts (section
+ * 7.1).  Returns -1 for a NULL net. */
 int64_t bp_num_weights(const bp_net* net);
 
-/* Copies n == bp_num_weights weights from host memory (layout above) and
- * zeroes the momentum.  Synchronous. */
+/* The state a net keeps between updates is its weights and the weight
+ * changes of the previous update (section 9; the update routine of section
+ * 6.2.1 reads both).  These four calls copy it between host memory (the
+ * caller's array of n == bp_num_weights floats, layout above) and the net.
+ * All are synchronous: they wait for the net's stream, then copy.
+ * BP_EINVAL for a NULL net or array, or n != bp_num_weights.
+ *
+ * bp_set_weights loads the weights and zeroes the momentum (a fresh start).
+ * bp_get_weights reads the current weights (it does not change the net). */
 int bp_set_weights(bp_net* net, const float* w_host, int64_t n);
+int bp_get_weights(const bp_net* net, float* w_host, int64_t n);
 
-/* Copies the n == bp_num_weights current weights to host memory.  Waits for
- * the net's stream.  Synchronous. */
-int bp_get_weights(bp_net* net, float* w_host, int64_t n);
-
-/* Momentum state V (the previous change, sections 6.2.1 and 9), same layout
- * as the weights.  Needed for an exact resume.  Synchronous. */
+/* Momentum state V (the previous change), same layout as the weights.
+ * Needed for an exact resume. */
 int bp_set_momentum(bp_net* net, const float* v_host, int64_t n);
-int bp_get_momentum(bp_net* net, float* v_host, int64_t n);
+int bp_get_momentum(const bp_net* net, float* v_host, int64_t n);
 
 /* One pass (epoch) over n_patterns dense patterns, in order, with one pooled
  * update per `batch` patterns (ceil(n_patterns / batch) updates; a short last
- * batch is applied like the others).  Momentum persists across batches and
- * calls.
+ * batch is applied like the others).  Each update is the paper's: forward
+ * pass, output and hidden deltas (section 3), the changes summed over the
+ * batch (section 4.1; section 3 allows pooling over fewer than all
+ * patterns), then learning rate and momentum applied to the sum (the update
+ * routine of section 6.2.1).  Momentum persists across batches and calls.
  *   inputs_dev  : float [n_patterns][n_0]
  *   targets_dev : float [n_patterns][n_L]
  *   batch >= 1; lr and momentum are used exactly as given (the change is the
@@ -103,9 +117,10 @@ int bp_train_batches(bp_net* net, const float* inputs_dev, const float* targets_
 /* As bp_train_batches, for inputs that are 0/1 with exactly n_active ones per
  * pattern (the NETtalk window coding: 7 positions x 29 symbols, section 6.3),
  * given as the indices of the ones:
- *   active_dev : int32 [n_patterns][n_active], each in [0, n_0), distinct
- *                within a pattern (not checked on the device: out-of-range
- *                indices are undefined behaviour).
+ *   active_dev : int32 [n_patterns][n_active], each in [0, n_0) and distinct
+ *                within a pattern.  An index outside [0, n_0) selects no
+ *                weight row (the pattern is treated as lacking that one);
+ *                duplicates are not detected.
  * The first layer gathers the n_active weight rows instead of multiplying;
  * its change touches only those rows, while the momentum term still moves
  * every row.  1 <= n_active <= n_0. */
@@ -113,8 +128,12 @@ int bp_train_batches_onehot(bp_net* net, const int32_t* active_dev, int32_t n_ac
                             const float* targets_dev, int64_t n_patterns, int32_t batch, float lr,
                             float momentum, double* sse_out);
 
-/* Forward pass only (no update): outputs_dev float [n_patterns][n_L] receives
- * the output activations for inputs_dev float [n_patterns][n_0]. */
+/* Forward pass only (no update; section 3: each unit applies the logistic to
+ * the weighted sum of the units feeding it and the true unit): outputs_dev
+ * float [n_patterns][n_L] receives the output activations for inputs_dev
+ * float [n_patterns][n_0] (both device memory, caller-owned).  Enqueued on
+ * the net's stream; returns without waiting.  BP_EINVAL for a NULL pointer
+ * (n_patterns > 0) or n_patterns outside [0, 2^31). */
 int bp_forward(bp_net* net, const float* inputs_dev, int64_t n_patterns, float* outputs_dev);
 
 /* Forward pass only for one-hot inputs given as active indices (see

@@ -938,7 +938,10 @@ __global__ __launch_bounds__(kThreads) void onehot_forward_kernel(const int32_t*
   if (p < rows && col < H) {
     float net = W0[(size_t)n0 * ldw + col];
     const int32_t* a = act + (size_t)p * n_active;
-    for (int k = 0; k < n_active; ++k) net += W0[(size_t)a[k] * ldw + col];
+    for (int k = 0; k < n_active; ++k) {
+      const int ix = a[k];   // an index outside [0, n0) selects no row
+      if ((unsigned)ix < (unsigned)n0) net += W0[(size_t)ix * ldw + col];
+    }
     const float y = unit_sigma(net, tab);
     if (mode == 0) {
       out[(size_t)p * ldo + col] = y;

@@ -107,20 +107,20 @@ struct bp_net {
   hipStream_t cap_stream = nullptr;
   hipGraph_t graph = nullptr;
   hipGraphExec_t graph_exec = nullptr;
-  std::string err;
+  mutable std::string err;            // message of the last failure (read-only calls set it too)
 };
 
 namespace {
 
 thread_local std::string g_create_err;
 
-int fail(bp_net* net, int code, const std::string& msg) {
+int fail(const bp_net* net, int code, const std::string& msg) {
   if (net) net->err = msg;
   else g_create_err = msg;
   return code;
 }
 
-int hip_fail(bp_net* net, hipError_t e, const char* what) {
+int hip_fail(const bp_net* net, hipError_t e, const char* what) {
   char buf[256];
   std::snprintf(buf, sizeof(buf), "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
   return fail(net, e == hipErrorOutOfMemory ? BP_ENOMEM : BP_EDEVICE, buf);
@@ -249,7 +249,7 @@ float* wbias(bp_net* net, int l) { return wl(net, l) + (size_t)net->n[l] * net->
 float* vbias(bp_net* net, int l) { return vl(net, l) + (size_t)net->n[l] * net->ldw[l]; }
 
 // Copies between the flat ABI layout (host) and the padded device layout.
-int copy_layers(bp_net* net, float* dev, const float* host_src, float* host_dst) {
+int copy_layers(const bp_net* net, float* dev, const float* host_src, float* host_dst) {
   for (int l = 0; l < net->L; ++l) {
     const size_t rows = (size_t)net->n[l] + 1, cols = (size_t)net->n[l + 1];
     float* d = dev + net->woff[l];
@@ -755,7 +755,7 @@ int checkpoint_restore(bp_net* net) {
   return BP_OK;
 }
 
-int check_net(bp_net* net) { return net ? BP_OK : BP_EINVAL; }
+int check_net(const bp_net* net) { return net ? BP_OK : BP_EINVAL; }
 
 }  // namespace
 
@@ -850,7 +850,7 @@ int bp_set_weights(bp_net* net, const float* w_host, int64_t n) {
   return copy_layers(net, net->W, w_host, nullptr);
 }
 
-int bp_get_weights(bp_net* net, float* w_host, int64_t n) {
+int bp_get_weights(const bp_net* net, float* w_host, int64_t n) {
   if (check_net(net)) return BP_EINVAL;
   if (!w_host) return fail(net, BP_EINVAL, "bp_get_weights: w_host is NULL");
   if (n != net->nweights) return fail(net, BP_EINVAL, "bp_get_weights: n != bp_num_weights");
@@ -865,7 +865,7 @@ int bp_set_momentum(bp_net* net, const float* v_host, int64_t n) {
   return copy_layers(net, net->V, v_host, nullptr);
 }
 
-int bp_get_momentum(bp_net* net, float* v_host, int64_t n) {
+int bp_get_momentum(const bp_net* net, float* v_host, int64_t n) {
   if (check_net(net)) return BP_EINVAL;
   if (!v_host) return fail(net, BP_EINVAL, "bp_get_momentum: v_host is NULL");
   if (n != net->nweights) return fail(net, BP_EINVAL, "bp_get_momentum: n != bp_num_weights");

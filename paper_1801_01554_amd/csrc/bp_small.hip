@@ -151,6 +151,9 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
 #pragma unroll
     for (int u = 0; u < 8; ++u) iv[g][u] = ip[min(u, n_active - 1)];
   }
+  // an index outside [0, n0) selects no row: it reads the bias row (always
+  // valid) and adds nothing
+  const unsigned n0u = (unsigned)n0;
   // Staging round (np * O <= 512 and P * OP <= 512 <= kT by the path's
   // limits).  Every load reads a clamped, valid address and is stored to LDS
   // unconditionally (the value selected; lanes past the end store to a spare
@@ -174,7 +177,7 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
   for (int g = 0; g < NG; ++g) {
     const int jc = min((tid + g * kT) & (HP - 1), H - 1);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) gv[g][u] = W0[(size_t)iv[g][u] * ldw0 + jc];
+    for (int u = 0; u < 8; ++u) gv[g][u] = W0[(size_t)((unsigned)iv[g][u] < n0u ? iv[g][u] : n0) * ldw0 + jc];
     gb[g] = W0[(size_t)n0 * ldw0 + jc];
   }
   {
@@ -198,9 +201,12 @@ __global__ __launch_bounds__(kT) void small_fwdbwd_kernel(const int32_t* __restr
       float net = gb[g];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (u < n_active) net += gv[g][u];
+        if (u < n_active && (unsigned)iv[g][u] < n0u) net += gv[g][u];
       const int32_t* ip = act + (size_t)(p0 + p) * n_active;
-      for (int k = 8; k < n_active; ++k) net += W0[(size_t)ip[k] * ldw0 + jc];
+      for (int k = 8; k < n_active; ++k) {
+        const int ix = ip[k];
+        if ((unsigned)ix < n0u) net += W0[(size_t)ix * ldw0 + jc];
+      }
       const float h = TAB ? logistic_table(net, tab) : logistic(net);
       hs[t] = j < H ? h : 0.f;
     }

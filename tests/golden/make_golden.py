@@ -1,6 +1,5 @@
 """Writes the stored expected values under tests/golden/ (calls only the oracle).
 
-    python tests/golden/make_golden.py worked            # 2-2-1 worked example
     python tests/golden/make_golden.py epoch NAME [...]   # full-epoch errors of a named workload
 
 Every number written here comes from ``oracle/`` on inputs from the seeded
@@ -19,37 +18,6 @@ sys.path.insert(0, ROOT)
 
 import oracle  # noqa: E402
 from paper_1801_01554_amd import workloads as wl  # noqa: E402
-
-# A 2-2-1 net, two patterns in one batch, two consecutive updates.
-WORKED = {
-    "sizes": [2, 2, 1],
-    "weights": [0.1, -0.2, 0.3, 0.4, 0.0, 0.1, 0.5, -0.6, 0.2],
-    "inputs": [[1.0, 0.0], [0.0, 1.0]],
-    "targets": [[0.9], [0.1]],
-    "lr": 0.5,
-    "momentum": 0.9,
-    "batch": 2,
-}
-
-
-def worked():
-    c = WORKED
-    net = oracle.OracleNet(c["sizes"], 64)
-    net.set_weights(np.array(c["weights"], np.float64))
-    x = np.array(c["inputs"], np.float32)
-    t = np.array(c["targets"], np.float32)
-    steps = []
-    for _ in range(2):
-        y = net.forward(x)[:, 0].tolist()
-        sse = net.train_epoch(t, c["batch"], c["lr"], c["momentum"], x=x)
-        steps.append({"outputs_before": y, "sse": sse, "weights_after": net.get_weights().tolist(),
-                      "momentum_after": net.get_momentum().tolist()})
-    out = dict(c, steps=steps,
-               source="oracle/ (double storage) via tests/golden/make_golden.py worked")
-    # The float inputs 0.9 / 0.1 are rounded to float32 before use.
-    with open(os.path.join(HERE, "worked_2_2_1.json"), "w") as f:
-        json.dump(out, f, indent=1)
-    print("wrote worked_2_2_1.json")
 
 
 def epoch(name, storages=(64, 32)):
@@ -84,9 +52,7 @@ def epoch(name, storages=(64, 32)):
 
 if __name__ == "__main__":
     what = sys.argv[1]
-    if what == "worked":
-        worked()
-    elif what == "epoch":
+    if what == "epoch":
         for nm in sys.argv[2:]:
             epoch(nm)
     else:

@@ -74,6 +74,7 @@ def test_first_window_matches_oracle(dev, name):
     ev = rel_maxabs(w.sizes, net.get_momentum(), o.get_momentum())
     _say(f"  weights rel err {ew}, momentum {ev}, sse {sg} vs {so}")
     assert max(ew) <= W_TOL
+    assert max(ev) <= W_TOL, ev
     assert rel(sg, so) <= SSE_TOL
 
 

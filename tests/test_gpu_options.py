@@ -99,8 +99,10 @@ def test_table_update_matches_oracle(dev, sizes, n, batch, onehot):
     net, o = _pair(w, table=True)
     sg, so = _epoch(net, o, w, dev, batch, 0.1, 0.9)
     ew = rel_maxabs(w.sizes, net.get_weights(), o.get_weights())
-    _say(f"  weights rel err {ew}, sse {sg} vs {so}")
+    ev = rel_maxabs(w.sizes, net.get_momentum(), o.get_momentum())
+    _say(f"  weights rel err {ew}, momentum {ev}, sse {sg} vs {so}")
     assert max(ew) <= W_TOL
+    assert max(ev) <= W_TOL, ev
     assert rel(sg, so) <= SSE_TOL
 
 
@@ -159,6 +161,7 @@ def test_fault_count_poisoned_target(dev, sizes, n, batch, onehot, poison):
     ev = rel_maxabs(w.sizes, net.get_momentum(), o.get_momentum())
     _say(f"  weights rel err {ew}, momentum {ev}")
     assert max(ew) <= W_TOL
+    assert max(ev) <= W_TOL, ev
     assert np.all(np.isfinite(net.get_weights()))
 
 

@@ -70,6 +70,7 @@ def _check_update(w, dev, batch, lr, mom, n=None, what=""):
     ev = rel_maxabs(w.sizes, vg, o.get_momentum())
     _say(f"  weights rel err per layer {ew}, momentum {ev}, sse gpu {sse_g} oracle {sse_o}")
     assert max(ew) <= W_TOL, ew
+    assert max(ev) <= W_TOL, ev
     if n > 0:
         assert rel(sse_g, sse_o) <= SSE_TOL
     net.close()
@@ -216,6 +217,37 @@ def test_onehot_path_equals_dense_path(dev):
     s2 = n2.train_batches(t, w.batch, w.lr, w.momentum, inputs=x)
     assert rel(s1, s2) <= 1e-5
     assert max(rel_maxabs(w.sizes, n1.get_weights(), n2.get_weights())) <= W_TOL
+
+
+# Out-of-range one-hot indices select no weight row: training and the
+# forward pass equal the oracle's dense path on the 0/1 inputs without them.
+@pytest.mark.parametrize("sizes,n,batch", [((203, 120, 26), 300, 100),    # fused small-net path
+                                           ((203, 300, 26), 200, 200)])   # gather + scatter kernels
+def test_onehot_out_of_range_indices_select_nothing(dev, sizes, n, batch):
+    w = wl.make_custom(sizes, n, seed=5 + n, onehot=True, init="uniform0.3")
+    act = w.active.copy()
+    g = np.random.default_rng(n)
+    bad = g.random(act.shape) < 0.15
+    act[bad] = g.choice(np.array([-1, -7, -2 ** 31, sizes[0], sizes[0] + 1, 2 ** 31 - 1], np.int32), int(bad.sum()))
+    x = np.zeros((n, sizes[0]), np.float32)
+    rows, cols = np.nonzero(~bad)
+    x[rows, act[rows, cols]] = 1.0
+    _say(f"case onehot out-of-range sizes={sizes} n={n} batch={batch} bad={int(bad.sum())}")
+    net = bp.Net(sizes)
+    net.set_weights(w.weights)
+    a = torch.from_numpy(act).to(dev)
+    y = net.forward(active=a).cpu().numpy()
+    sse_g = net.train_batches(torch.from_numpy(w.targets).to(dev), batch, 0.05, 0.9, active=a)
+    o = _oracle_net(w)
+    ref_y = o.forward(x=x)
+    sse_o = o.train_epoch(w.targets, batch, 0.05, 0.9, x=x)
+    ew = rel_maxabs(sizes, net.get_weights(), o.get_weights())
+    ev = rel_maxabs(sizes, net.get_momentum(), o.get_momentum())
+    _say(f"  forward err {np.max(np.abs(y - ref_y))}, weights {ew}, momentum {ev}, sse {sse_g} vs {sse_o}")
+    assert np.max(np.abs(y - ref_y)) <= FWD_TOL
+    assert max(ew) <= W_TOL and max(ev) <= W_TOL
+    assert rel(sse_g, sse_o) <= SSE_TOL
+    net.close()
 
 
 @pytest.mark.parametrize("name,n", [("nettalk-120-b512", 2048), ("deep-512-2048x3-64", 8192)])
