@@ -50,13 +50,13 @@ PRIMARY = "deep-512-2048x3-64"
 SECONDARY = ("wide-1024-4096-1024", "nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16")
 VARIANT_WORKLOAD = "nettalk-120-b512"
 SECONDARY_SEQ = ("elman-64+256-256-64",)
-GEMM_KINDS = ("forward", "output", "backward", "change", "seq_pair")
+GEMM_KINDS = ("forward", "output", "backward", "change", "splitk", "seq_pair")
 KERNEL_NAMES = {
     "forward": "gemm_kernel|skinny_kernel<..., EpiSigmoid>",
     "output": "gemm_kernel|skinny_kernel<..., EpiOutputDelta>",
     "backward": "gemm_kernel|skinny_kernel<..., EpiHiddenDelta>",
-    "change": "gemm_kernel|skinny_kernel<..., EpiUpdate|EpiPartial>",
-    "splitk": "splitk_update_kernel",
+    "change": "gemm_kernel<..., EpiUpdate>",
+    "splitk": "gemm_kernel|skinny_kernel<..., EpiSplitUpdate>",
     "bias": "bias_update_kernel",
     "gather": "onehot_forward_kernel",
     "scatter": "onehot_update_kernel",
@@ -105,8 +105,7 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
                 add("forward", 2 * R * ni * no, 4 * (R * ni + (ni + 1) * no + R * no))
             upd = 16.0 * ni * no
             if bwd and splits_of(ni, no, rows) > 1:
-                add("change", 2 * R * ni * no, 4 * (R * ni + R * no))
-                add("splitk", 0.0, upd)
+                add("splitk", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
             elif bwd:
                 add("change", 2 * R * ni * no, 4 * (R * ni + R * no) + upd)
             if bwd:
@@ -173,10 +172,11 @@ def elman_pair(sizes, n_ctx, S):
 
 
 def change_splits(M, N, K):
-    """Mirror of the library's split count for a change product, for work accounting only."""
+    """Mirror of the library's split count for a change product (split over blocks, whose last
+    block per tile applies the update), for work accounting only."""
     if K >= 1024 and -(-M // 64) * -(-N // 64) < 128:
         tiles, chunk = -(-M // 64) * -(-N // 32), 1024
-        while chunk > 128 and tiles * -(-K // chunk) < 512:
+        while chunk > 128 and tiles * -(-K // chunk) < 256:
             chunk //= 2
         if -(-K // chunk) >= 2:
             return -(-K // chunk)
@@ -427,13 +427,13 @@ def kind_of_kernel(name):
     if m:
         epi = m.group(5)
         if epi == "EpiPartial":
-            return "change" if m.group(1) == "true" else "output"
+            return "output"
         return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
-                "EpiUpdate": "change"}.get(epi)
+                "EpiUpdate": "change", "EpiSplitUpdate": "splitk"}.get(epi)
     m = re.search(r"skinny_kernel<\d+, [^>]*?(\w+)>", name)
     if m:
         return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
-                "EpiPartial": "change"}.get(m.group(1))
+                "EpiSplitUpdate": "splitk"}.get(m.group(1))
     for k, v in KERNEL_NAMES.items():
         if "<" not in v and v in name:
             return k

@@ -237,8 +237,10 @@ enum {
   BP_K_FORWARD = 0,   /* hidden-layer forward product + sigmoid            */
   BP_K_OUTPUT = 1,    /* output-layer forward product + deltas + error      */
   BP_K_BACKWARD = 2,  /* hidden-delta product + derivative                  */
-  BP_K_CHANGE = 3,    /* summed-change product (+ momentum update)          */
-  BP_K_SPLITK = 4,    /* ordered split-K reduction + momentum update        */
+  BP_K_CHANGE = 3,    /* summed-change product + momentum update           */
+  BP_K_SPLITK = 4,    /* summed-change product split over the batch; the  */
+                      /* last block of each tile adds the partials in     */
+                      /* split order and applies the momentum update      */
   BP_K_BIAS = 5,      /* bias-row column sums + momentum update             */
   BP_K_GATHER = 6,    /* one-hot first-layer forward                        */
   BP_K_SCATTER = 7,   /* one-hot first-layer change + momentum update       */

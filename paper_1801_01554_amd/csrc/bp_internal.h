@@ -101,23 +101,30 @@ hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W
                           int K, const float* act, int lda, float* out, int ldo, float* colsum, int ldcs);
 
 // Number of K-splits change_update uses for an M x N change summed over K
-// rows (1 = the product applies the update itself).
+// rows (1 = one block per output tile applies the update from its
+// accumulators).
 int change_splits(int M, int N, int K);
 
 // Floats of split workspace change_update needs for an M x N change summed over K rows.
 size_t change_update_workspace(int M, int N, int K);
 
+// Arrival counters (one per output tile) a split change_update of an M x N
+// change summed over K rows uses; 0 when it is not split.  Never more than
+// kMaxArrivals: a product is split only when it has fewer output tiles than
+// that.
+constexpr int kMaxArrivals = 512;
+int change_arrivals(int M, int N, int K);
+
 // Weight change and update for the non-bias rows:
 //   G[m][n] = sum_k A[k][m] D[k][n];  V = lr G + mom V;  W += V   (m < M, n < N).
-// With change_splits(M, N, K) > 1 this launch only writes the partial sums
-// to `ws` (change_update_workspace floats) and splitk_finish must follow.
+// With change_splits(M, N, K) > 1 the blocks of each output tile write their
+// partial sums to `ws` (change_update_workspace floats) and the last one to
+// arrive adds them in split order and applies the update, counting arrivals
+// in `arrivals` (kMaxArrivals ints, all zero before the launch and left zero
+// after it; launches that use them must not overlap).
 hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N,
-                         int K, float* W, float* V, int ldw, float lr, float mom, float* ws, float limit,
-                         unsigned long long* faults);
-
-// Sums the split partials of change_update in split order, then updates V and W.
-hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
-                         const float* ws, float limit, unsigned long long* faults);
+                         int K, float* W, float* V, int ldw, float lr, float mom, float* ws, int* arrivals,
+                         float limit, unsigned long long* faults);
 
 // Bias-row change and update: G[n] = sum_{k < rows} D[k][n];  V = lr G + mom V;  W += V.
 // D is the per-tile column-sum buffer of the deltas (rows = colsum_rows(batch)).

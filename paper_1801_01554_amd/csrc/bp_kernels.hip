@@ -157,6 +157,98 @@ struct EpiPartial {
   }
 };
 
+// Split-K change product fused with the update (the update routine of
+// section 6.2.1 applied to the batch-summed change).  The blocks of one
+// output tile each sum one K range of the batch.  Every block stores its
+// partial sums and counts its arrival (one counter per output tile); the
+// block that arrives last adds the tile's partials in split order, taking
+// its own from registers, and applies the range check and the momentum
+// update to them, as the epilogue of an unsplit product does.  The sum does
+// not depend on which block arrives last (results are run-to-run identical)
+// and the summed change itself never reaches memory.
+//
+// Partials are stored in the accumulator layout, lane fastest: 4-float slot
+// u of lane l in wave w of block (tile t, split z) is at float offset
+//   (((z * tiles + t) * waves + w) * slots + u) * 256 + 4 l,
+// so every store or load instruction of a wave covers 1 KB of contiguous
+// memory.  They are written and read with the device-coherent cache policy
+// (written through the L2 of the XCD, read from the coherent level), so
+// blocks on different XCDs see each other's partials without a fence (a
+// device-scope fence would write back, or drop, the whole L2 of the XCD).
+struct EpiSplitUpdate {
+  float* P;                         // partials (split_workspace floats)
+  float* W;
+  float* V;
+  int ldw;
+  float lr, mom;
+  float limit;                      // range check of the summed change (> 0: on)
+  unsigned long long* faults;
+  int* arrivals;                    // per output tile; zero before and after every launch
+  int splits;
+  static constexpr bool kColSum = false;
+  static constexpr bool kFaults = true;
+};
+
+constexpr int kCoherent = 16;       // buffer cache policy bit sc1: device-coherent access
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t partial_rsrc(float* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, 0x7fffffff, 0x00020000);
+}
+
+// Every thread of the block calls this after storing its partial slots.
+// Each wave waits until its stores are complete (performed at the coherent
+// level) before the block's arrival is counted.  Returns true, in every
+// thread, in the block that arrives last at `tile`; that block also resets
+// the tile's counter for the next launch.
+__device__ __forceinline__ bool split_arrive(const EpiSplitUpdate& e, int tile) {
+  __shared__ int last;
+  __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's partial stores are complete
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const bool l =
+        __hip_atomic_fetch_add(e.arrivals + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == e.splits - 1;
+    if (l) __hip_atomic_store(e.arrivals + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last = l;
+  }
+  __syncthreads();
+  return last;
+}
+
+// g[u] = the sum over splits 0 .. S-1, in split order, of this lane's slot
+// `slot0 + u` (split z's own value from `own`).  `r` addresses split 0 of
+// the block's partials; splits are `zstride` bytes apart, slots 1 KB.  The
+// other splits' slots are loaded in groups, all in flight together: one
+// split at a time for 4 slots (a 32 x 32 block of gemm_kernel: more would
+// cost it its second wave per SIMD), 16 splits for one slot.
+template <int NS>
+__device__ __forceinline__ void ordered_split_sum(f32x4 (&g)[NS], const f32x4 (&own)[NS], __amdgpu_buffer_rsrc_t r,
+                                                  int zstride, int slot0, int lane, int z, int S) {
+  constexpr int ZB = NS >= 4 ? 1 : 16 / NS;   // splits per load group
+#pragma unroll
+  for (int u = 0; u < NS; ++u) g[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int z0 = 0; z0 < S; z0 += ZB) {
+    f32x4 t[ZB][NS];
+#pragma unroll
+    for (int d = 0; d < ZB; ++d) {
+      const int zz = z0 + d;
+      if (zz < S && zz != z) {
+#pragma unroll
+        for (int u = 0; u < NS; ++u)
+          t[d][u] = __builtin_amdgcn_raw_buffer_load_b128(r, zz * zstride + ((slot0 + u) * 64 + lane) * 16, 0,
+                                                          kCoherent);
+      }
+    }
+#pragma unroll
+    for (int d = 0; d < ZB; ++d) {
+      const int zz = z0 + d;
+      if (zz < S) {
+#pragma unroll
+        for (int u = 0; u < NS; ++u) g[u] += zz == z ? own[u] : t[d][u];
+      }
+    }
+  }
+}
+
 // --------------------------------------------------------------------------
 // Tiled fp32 MFMA product C[M][N] = sum_k A(m, k) B(k, n).
 //
@@ -186,12 +278,12 @@ struct Tile {
 // registers; elements outside [0, O_lim) x [0, D_lim) read as zero.
 template <int TO, int TD, bool VEC>
 __device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld, int o0, int d0, int O_lim,
-                                          int D_lim, f32x4* r) {
+                                          int D_lim, f32x4* r, int tid) {
   constexpr int PER = TO * TD / 4 / kThreads;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = threadIdx.x + q * kThreads;
+    const int f = tid + q * kThreads;
     const int go = o0 + f / D4, gd = d0 + (f % D4) * 4;
     f32x4 v = {0.f, 0.f, 0.f, 0.f};
     if (go < O_lim) {
@@ -211,23 +303,24 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld
 // Loads a TO x TD tile that lies entirely inside the matrix, 16 bytes per
 // load, with no bounds checks (interior tiles of 16-byte aligned operands).
 template <int TO, int TD>
-__device__ __forceinline__ void load_tile_full(const float* __restrict__ base, int ld, int o0, int d0, f32x4* r) {
+__device__ __forceinline__ void load_tile_full(const float* __restrict__ base, int ld, int o0, int d0, f32x4* r,
+                                               int tid) {
   constexpr int PER = TO * TD / 4 / kThreads;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = threadIdx.x + q * kThreads;
+    const int f = tid + q * kThreads;
     r[q] = *reinterpret_cast<const f32x4*>(base + (size_t)(o0 + f / D4) * ld + d0 + (f % D4) * 4);
   }
 }
 
 template <int TO, int TD, int S>
-__device__ __forceinline__ void store_tile(float* lds, const f32x4* r) {
+__device__ __forceinline__ void store_tile(float* lds, const f32x4* r, int tid) {
   constexpr int PER = TO * TD / 4 / kThreads;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = threadIdx.x + q * kThreads;
+    const int f = tid + q * kThreads;
     *reinterpret_cast<f32x4*>(lds + (f / D4) * S + (f % D4) * 4) = r[q];
   }
 }
@@ -261,10 +354,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   int tm, tn;
   xcd_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x;
   const int kb = blockIdx.z * k_chunk;
   const int ke = min(K, kb + k_chunk);
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = tid >> 6, lane = tid & 63;
   const int wm0 = (wave >> 1) * T::WM, wn0 = (wave & 1) * T::WN;
   const int r = lane & 31, h = lane >> 5;
 
@@ -285,25 +379,25 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   auto load_stage = [&](int k, f32x4* ra, f32x4* rb) {
     const bool k_in = k + BK <= ke;
     if (AVEC && a_rows_in && k_in) {
-      if (A_KM) load_tile_full<BK, BM>(A, lda, k, m0, ra);
-      else load_tile_full<BM, BK>(A, lda, m0, k, ra);
+      if (A_KM) load_tile_full<BK, BM>(A, lda, k, m0, ra, tid);
+      else load_tile_full<BM, BK>(A, lda, m0, k, ra, tid);
     } else {
-      if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra);
-      else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra);
+      if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra, tid);
+      else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra, tid);
     }
     if (BVEC && b_rows_in && k_in) {
-      if (B_NK) load_tile_full<BN, BK>(B, ldb, n0, k, rb);
-      else load_tile_full<BK, BN>(B, ldb, k, n0, rb);
+      if (B_NK) load_tile_full<BN, BK>(B, ldb, n0, k, rb, tid);
+      else load_tile_full<BK, BN>(B, ldb, k, n0, rb, tid);
     } else {
-      if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb);
-      else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb);
+      if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb, tid);
+      else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb, tid);
     }
   };
   auto store_stage = [&](int buf, const f32x4* ra, const f32x4* rb) {
-    if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra);
-    else store_tile<BM, BK, T::SA>(As[buf], ra);
-    if (B_NK) store_tile<BN, BK, T::SB>(Bs[buf], rb);
-    else store_tile<BK, BN, T::SB>(Bs[buf], rb);
+    if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra, tid);
+    else store_tile<BM, BK, T::SA>(As[buf], ra, tid);
+    if (B_NK) store_tile<BN, BK, T::SB>(Bs[buf], rb, tid);
+    else store_tile<BK, BN, T::SB>(Bs[buf], rb, tid);
   };
   auto compute = [&](int buf) {
     const float* as = As[buf];
@@ -365,71 +459,125 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
-  float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
-  // The per-element operands of each 32 x 32 block are loaded together
-  // (clamped, always valid addresses; values outside the matrix are never
-  // used) before the block's stores: one memory round trip per block, with
-  // few extra registers.
-  float csum[T::TN];
+  if constexpr (std::is_same_v<Epi, EpiSplitUpdate>) {
+    // The block's partial (slot (i TN + j) 4 + q of a wave = registers 4 q
+    // .. 4 q + 3 of block (i, j)), its arrival, and in the last block of the
+    // tile the ordered sum of the splits and the update.
+    constexpr int kSlots = T::TM * T::TN * 4;
+    const int tile = tm * tiles_n + tn;
+    const int zstride = tiles_m * tiles_n * BM * BN * 4;
+    const __amdgpu_buffer_rsrc_t pr = partial_rsrc(epi.P + (size_t)tile * BM * BN + wave * kSlots * 256);
+    const int z = blockIdx.z;
 #pragma unroll
-  for (int j = 0; j < T::TN; ++j) {
-    csum[j] = 0.f;
-    const int n = n0 + wn0 + j * 32 + r;
-    if (n < N) {
-      const float cv = epi.column(n);
+    for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-      for (int i = 0; i < T::TM; ++i) {
-        typename Epi::Pre pre[16];
+      for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          pre[e] = epi.load(min(m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), M - 1), n);
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          __builtin_amdgcn_raw_buffer_store_b128(v, pr, z * zstride + (((i * T::TN + j) * 4 + q) * 64 + lane) * 16, 0,
+                                                 kCoherent);
+        }
+    if (!split_arrive(epi, tile)) return;
+    int nf = 0;
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int n = n0 + wn0 + j * 32 + r, nc = min(n, N - 1);
+        float vo[16], wo[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-          if (m < M) csum[j] += epi.apply(m, n, acc[i][j][e], cv, pre[e], sse);
+          const size_t idx = (size_t)min(m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), M - 1) * epi.ldw + nc;
+          vo[e] = epi.V[idx];
+          wo[e] = epi.W[idx];
+        }
+        f32x4 own[4], g[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          own[q] = f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        ordered_split_sum<4>(g, own, pr, zstride, (i * T::TN + j) * 4, lane, z, epi.splits);
+        if (n < N) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+            if (m < M) {
+              const size_t idx = (size_t)m * epi.ldw + n;
+              const float v = momentum_step(checked_change(g[e >> 2][e & 3], epi.limit, nf), vo[e], epi.lr, epi.mom);
+              epi.V[idx] = v;
+              epi.W[idx] = wo[e] + v;
+            }
+          }
+        }
+      }
+    if (epi.limit > 0.f) add_faults(nf, epi.faults);
+  } else {
+    float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
+    // The per-element operands of each 32 x 32 block are loaded together
+    // (clamped, always valid addresses; values outside the matrix are never
+    // used) before the block's stores: one memory round trip per block, with
+    // few extra registers.
+    float csum[T::TN];
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j) {
+      csum[j] = 0.f;
+      const int n = n0 + wn0 + j * 32 + r;
+      if (n < N) {
+        const float cv = epi.column(n);
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i) {
+          typename Epi::Pre pre[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            pre[e] = epi.load(min(m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), M - 1), n);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+            if (m < M) csum[j] += epi.apply(m, n, acc[i][j][e], cv, pre[e], sse);
+          }
         }
       }
     }
-  }
-  if constexpr (Epi::kColSum) {
-    // Column sums per 64-row group of the tile (a 128-row tile has two, one
-    // per wave row; a 64-row tile one, over both wave rows).  Lanes h = 0, 1
-    // hold the same column (different rows); the wave rows of a group are
-    // then added in a fixed order.
-    static_assert(BM == 64 || BM == 128, "column-sum groups assume 64- or 128-row tiles");
-    constexpr int kGroups = BM / 64, kWaveRowsPerGroup = 2 / kGroups;
-    __shared__ float cs[2][BN];
+    if constexpr (Epi::kColSum) {
+      // Column sums per 64-row group of the tile (a 128-row tile has two, one
+      // per wave row; a 64-row tile one, over both wave rows).  Lanes h = 0, 1
+      // hold the same column (different rows); the wave rows of a group are
+      // then added in a fixed order.
+      static_assert(BM == 64 || BM == 128, "column-sum groups assume 64- or 128-row tiles");
+      constexpr int kGroups = BM / 64, kWaveRowsPerGroup = 2 / kGroups;
+      __shared__ float cs[2][BN];
 #pragma unroll
-    for (int j = 0; j < T::TN; ++j) {
-      const float v = csum[j] + __shfl_xor(csum[j], 32, 64);
-      if (h == 0) cs[wave >> 1][wn0 + j * 32 + r] = v;
-    }
-    __syncthreads();
+      for (int j = 0; j < T::TN; ++j) {
+        const float v = csum[j] + __shfl_xor(csum[j], 32, 64);
+        if (h == 0) cs[wave >> 1][wn0 + j * 32 + r] = v;
+      }
+      __syncthreads();
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-      const int crow = tm * kGroups + g;
-      if (crow * 64 >= M) break;
-      for (int c = threadIdx.x; c < BN; c += kThreads) {
-        if (n0 + c >= N) continue;
-        float v = cs[g * kWaveRowsPerGroup][c];
-        for (int w = 1; w < kWaveRowsPerGroup; ++w) v += cs[g * kWaveRowsPerGroup + w][c];
-        epi.colsum[(size_t)crow * epi.ldcs + n0 + c] = v;
+      for (int g = 0; g < kGroups; ++g) {
+        const int crow = tm * kGroups + g;
+        if (crow * 64 >= M) break;
+        for (int c = threadIdx.x; c < BN; c += kThreads) {
+          if (n0 + c >= N) continue;
+          float v = cs[g * kWaveRowsPerGroup][c];
+          for (int w = 1; w < kWaveRowsPerGroup; ++w) v += cs[g * kWaveRowsPerGroup + w][c];
+          epi.colsum[(size_t)crow * epi.ldcs + n0 + c] = v;
+        }
       }
     }
-  }
-  if constexpr (Epi::kFaults) {
-    if (epi.limit > 0.f) add_faults((int)sse, epi.faults);
-  }
-  if constexpr (Epi::kSSE) {
-    __shared__ float red[kThreads / 64];
+    if constexpr (Epi::kFaults) {
+      if (epi.limit > 0.f) add_faults((int)sse, epi.faults);
+    }
+    if constexpr (Epi::kSSE) {
+      __shared__ float red[kThreads / 64];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
-    if (lane == 0) red[wave] = sse;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      double s = 0.0;
-      for (int w = 0; w < kThreads / 64; ++w) s += (double)red[w];
-      epi.sse_part[blockIdx.x] = s;
+      for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+      if (lane == 0) red[wave] = sse;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        double s = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) s += (double)red[w];
+        epi.sse_part[blockIdx.x] = s;
+      }
     }
   }
 }
@@ -494,12 +642,13 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 // row block are added through LDS in K order, and the four waves of the row
 // block share its epilogue (RB = 2 for epilogues with 64-row column sums).
 //
-// With EpiPartial the kernel is a split-K change product (section 6.2.1, the
-// batch-summed change of one layer's weights when the batch is long and the
-// layer small): A is stored k-major (A[k][m], the activations), the block
-// covers K range [z k_chunk, (z + 1) k_chunk) of split z and writes raw
-// partial sums for splitk_finish.  Blocks are ordered split-major and handed
-// to the XCDs in contiguous ranges, so each XCD reads one K range of both
+// With EpiSplitUpdate the kernel is a split-K change product (section
+// 6.2.1, the batch-summed change of one layer's weights when the batch is
+// long and the layer small): A is stored k-major (A[k][m], the activations),
+// the block covers K range [z k_chunk, (z + 1) k_chunk) of split z and
+// stores its partial sums; the last block of each tile adds them in split
+// order and applies the update (EpiSplitUpdate).  Blocks are ordered split-major and handed to
+// the XCDs in contiguous ranges, so each XCD reads one K range of both
 // operands.
 //
 // With CTX, A is the input of an Elman step built on the fly (section 10.5):
@@ -529,8 +678,8 @@ __device__ __forceinline__ void skinny_body(int bid, int nblocks, float (&part)[
                                             const float* __restrict__ A, int lda, const float* __restrict__ B,
                                             int ldb, int M, int N, int K, int k_chunk, const Epi& epi,
                                             const CtxInput& ctx) {
-  constexpr bool SPLIT = std::is_same_v<Epi, EpiPartial>;
-  static_assert(!Epi::kFaults, "update epilogues take gemm_kernel");
+  constexpr bool SPLIT = std::is_same_v<Epi, EpiSplitUpdate>;
+  static_assert(!Epi::kFaults || SPLIT, "unsplit update epilogues take gemm_kernel");
   static_assert(!Epi::kColSum || RB == 2, "64-row column sums need RB = 2");
   static_assert(!A_KM || (SPLIT && !AVEC && !CTX), "k-major A is the change product's");
   constexpr int C = kSkinnyChunk;
@@ -678,53 +827,89 @@ __device__ __forceinline__ void skinny_body(int bid, int nblocks, float (&part)[
 #pragma unroll
   for (int e = 0; e < 16; ++e) part[kg][rb][e][lane] = acc[e];
   __syncthreads();
-  float sse = 0.f, csum = 0.f;
-  if (n < N) {
-    const float cv = epi.column(n);
-    float v[4];
-    typename Epi::Pre pre[4];
+  if constexpr (SPLIT) {
+    // One 4-float slot per thread (slot = wave): rows 8 kg + 4 h + q of row
+    // block rb, column n.  Then the arrival, and in the last block of the
+    // tile the ordered sum of the splits and the update.
+    f32x4 own[1], g[1];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * kg + q;
-      v[q] = ((part[0][rb][e][lane] + part[1][rb][e][lane]) + part[2][rb][e][lane]) + part[3][rb][e][lane];
-      pre[q] = epi.load(min(m0 + rb * 32 + 8 * kg + 4 * h + q, M - 1), n);
+      own[0][q] = ((part[0][rb][e][lane] + part[1][rb][e][lane]) + part[2][rb][e][lane]) + part[3][rb][e][lane];
     }
+    const int tile = tm * tiles_n + tn;
+    const int zstride = tiles_m * tiles_n * 32 * RB * 32 * 4;
+    const __amdgpu_buffer_rsrc_t pr = partial_rsrc(epi.P + (size_t)tile * 32 * RB * 32);
+    __builtin_amdgcn_raw_buffer_store_b128(own[0], pr, z * zstride + (wave * 64 + lane) * 16, 0, kCoherent);
+    if (!split_arrive(epi, tile)) return;
+    const int nc = min(n, N - 1);
+    float vo[4], wo[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int mm = m0 + rb * 32 + 8 * kg + 4 * h + q;
-      if constexpr (SPLIT) {
-        if (mm < M) epi.P[z * epi.split_stride + (size_t)mm * epi.ldp + n] = v[q];
-      } else {
+      const size_t idx = (size_t)min(m0 + rb * 32 + 8 * kg + 4 * h + q, M - 1) * epi.ldw + nc;
+      vo[q] = epi.V[idx];
+      wo[q] = epi.W[idx];
+    }
+    ordered_split_sum<1>(g, own, pr, zstride, wave, lane, z, epi.splits);
+    int nf = 0;
+    if (n < N) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int mm = m0 + rb * 32 + 8 * kg + 4 * h + q;
+        if (mm < M) {
+          const size_t idx = (size_t)mm * epi.ldw + n;
+          const float v = momentum_step(checked_change(g[0][q], epi.limit, nf), vo[q], epi.lr, epi.mom);
+          epi.V[idx] = v;
+          epi.W[idx] = wo[q] + v;
+        }
+      }
+    }
+    if (epi.limit > 0.f) add_faults(nf, epi.faults);
+  } else {
+    float sse = 0.f, csum = 0.f;
+    if (n < N) {
+      const float cv = epi.column(n);
+      float v[4];
+      typename Epi::Pre pre[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = 4 * kg + q;
+        v[q] = ((part[0][rb][e][lane] + part[1][rb][e][lane]) + part[2][rb][e][lane]) + part[3][rb][e][lane];
+        pre[q] = epi.load(min(m0 + rb * 32 + 8 * kg + 4 * h + q, M - 1), n);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int mm = m0 + rb * 32 + 8 * kg + 4 * h + q;
         if (mm < M) csum += epi.apply(mm, n, v[q], cv, pre[q], sse);
       }
     }
-  }
-  if constexpr (Epi::kColSum) {
-    // the 64-row tile's column sums: per wave over its 8 rows (lanes h = 0,
-    // 1 hold the same column), then the waves in (row block, K group) order
-    __shared__ float cs[2][4][32];
-    const float v = csum + __shfl_xor(csum, 32, 64);
-    if (h == 0) cs[rb][kg][r] = v;
-    __syncthreads();
-    if (threadIdx.x < 32 && n0 + (int)threadIdx.x < N) {
-      float t = 0.f;
+    if constexpr (Epi::kColSum) {
+      // the 64-row tile's column sums: per wave over its 8 rows (lanes h = 0,
+      // 1 hold the same column), then the waves in (row block, K group) order
+      __shared__ float cs[2][4][32];
+      const float v = csum + __shfl_xor(csum, 32, 64);
+      if (h == 0) cs[rb][kg][r] = v;
+      __syncthreads();
+      if (threadIdx.x < 32 && n0 + (int)threadIdx.x < N) {
+        float t = 0.f;
 #pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2)
+        for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) t += cs[b2][g][threadIdx.x];
-      epi.colsum[(size_t)tm * epi.ldcs + n0 + threadIdx.x] = t;
+          for (int g = 0; g < 4; ++g) t += cs[b2][g][threadIdx.x];
+        epi.colsum[(size_t)tm * epi.ldcs + n0 + threadIdx.x] = t;
+      }
     }
-  }
-  if constexpr (Epi::kSSE) {
-    __shared__ float red[4 * RB];
+    if constexpr (Epi::kSSE) {
+      __shared__ float red[4 * RB];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
-    if (lane == 0) red[wave] = sse;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      double s = 0.0;
-      for (int w = 0; w < 4 * RB; ++w) s += (double)red[w];
-      epi.sse_part[bid] = s;
+      for (int off = 32; off > 0; off >>= 1) sse += __shfl_xor(sse, off, 64);
+      if (lane == 0) red[wave] = sse;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        double s = 0.0;
+        for (int w = 0; w < 4 * RB; ++w) s += (double)red[w];
+        epi.sse_part[bid] = s;
+      }
     }
   }
 }
@@ -780,38 +965,6 @@ hipError_t launch_skinny(hipStream_t s, const float* A, int lda, const float* B,
                          ldb, M, N, K, K, epi, none);
   return launch_kernel(skinny_kernel<RB, false, B_NK, false, false, false, Epi>, tiles, 256 * RB, 0, s, A, lda, B, ldb,
                        M, N, K, K, epi, none);
-}
-
-// --------------------------------------------------------------------------
-// Split-K reduction of the change followed by the momentum update.
-__global__ __launch_bounds__(kThreads) void splitk_update_kernel(const float* __restrict__ P, int splits,
-                                                                 size_t split_stride, int M, int N, int ldp,
-                                                                 float* W, float* V, int ldw, float lr,
-                                                                 float mom, float limit,
-                                                                 unsigned long long* faults) {
-  const size_t idx = (size_t)blockIdx.x * kThreads + threadIdx.x;
-  int nf = 0;
-  if (idx < (size_t)M * N) {
-    const int m = (int)(idx / N), n = (int)(idx % N);
-    // eight partials in flight at a time, added in split order
-    const float* p = P + (size_t)m * ldp + n;
-    float g = 0.f;
-    int z = 0;
-    for (; z + 8 <= splits; z += 8) {
-      float v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = p[(z + e) * split_stride];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) g += v[e];
-    }
-    for (; z < splits; ++z) g += p[z * split_stride];
-    g = checked_change(g, limit, nf);
-    const size_t i = (size_t)m * ldw + n;
-    const float v = momentum_step(g, V[i], lr, mom);
-    V[i] = v;
-    W[i] = W[i] + v;
-  }
-  if (limit > 0.f) add_faults(nf, faults);
 }
 
 // Split-K output layer: sums the split partials in split order, then applies
@@ -1165,38 +1318,47 @@ hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W
 
 // The change product of a layer: few output tiles and a long batch take the
 // split-K skinny kernel (64 x 32 tiles), with the largest K chunk of 1024,
-// 512, 256 or 128 that still gives kSkinnyChangeBlocks blocks; the others
+// 512, 256 or 128 that still gives kSkinnyChangeBlocks blocks (one per CU:
+// every block pays the arrival's round trips once); the others
 // take gemm_kernel, split over K when the batch is long (choose_splits).
-constexpr int kSkinnyChangeBlocks = 512;
+// Split products apply the update in the last block of each tile
+// (EpiSplitUpdate); the others in every block's epilogue (EpiUpdate).
+constexpr int kSkinnyChangeBlocks = 256;
 struct ChangePlan {
   bool skinny;
   int splits;
   int chunk;
+  int tiles;        // output tiles
+  int tile_elems;   // floats per output tile
 };
 
 ChangePlan change_plan(int M, int N, int K) {
   if (K >= 1024 && tiles_of(M, N, 64) < 128) {
-    const long tiles = (long)((M + 63) / 64) * ((N + 31) / 32);
+    const int tiles = ((M + 63) / 64) * ((N + 31) / 32);
     int chunk = 1024;
-    while (chunk > 128 && tiles * ((K + chunk - 1) / chunk) < kSkinnyChangeBlocks) chunk /= 2;
+    while (chunk > 128 && (long)tiles * ((K + chunk - 1) / chunk) < kSkinnyChangeBlocks) chunk /= 2;
     const int sp = (K + chunk - 1) / chunk;
-    if (sp >= 2) return {true, sp, chunk};
+    if (sp >= 2) return {true, sp, chunk, tiles, 64 * 32};
   }
   const int sp = choose_splits(M, N, K);
-  return {false, sp, sp > 1 ? chunk_for(K, sp) : K};
+  const int t = tile_edge(M, N, K);
+  return {false, sp, sp > 1 ? chunk_for(K, sp) : K, tiles_of(M, N, t), t * t};
 }
 
 int change_splits(int M, int N, int K) { return change_plan(M, N, K).splits; }
 
 size_t change_update_workspace(int M, int N, int K) {
-  const int sp = change_splits(M, N, K);
-  if (sp <= 1) return 0;
-  const int ldp = (N + 3) / 4 * 4;
-  return (size_t)sp * M * ldp;
+  const ChangePlan pl = change_plan(M, N, K);
+  return pl.splits > 1 ? (size_t)pl.splits * pl.tiles * pl.tile_elems : 0;
+}
+
+int change_arrivals(int M, int N, int K) {
+  const ChangePlan pl = change_plan(M, N, K);
+  return pl.splits > 1 ? pl.tiles : 0;
 }
 
 hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D, int ldd, int M, int N, int K,
-                         float* W, float* V, int ldw, float lr, float mom, float* ws, float limit,
+                         float* W, float* V, int ldw, float lr, float mom, float* ws, int* arrivals, float limit,
                          unsigned long long* faults) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const ChangePlan pl = change_plan(M, N, K);
@@ -1204,24 +1366,12 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
     EpiUpdate e{W, V, ldw, lr, mom, limit, faults};
     return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, 1, K, e);
   }
-  const int ldp = (N + 3) / 4 * 4;
-  EpiPartial e{ws, ldp, (size_t)M * ldp};
-  if (pl.skinny) {
-    const int blocks = ((M + 63) / 64) * ((N + 31) / 32) * pl.splits;
-    return launch_kernel(skinny_kernel<2, true, false, false, false, false, EpiPartial>, blocks, 512, 0, s, A, lda, D,
-                         ldd, M, N, K, pl.chunk, e, CtxInput{});
-  }
+  if (!arrivals || !ws || pl.tiles > kMaxArrivals) return hipErrorInvalidValue;
+  EpiSplitUpdate e{ws, W, V, ldw, lr, mom, limit, faults, arrivals, pl.splits};
+  if (pl.skinny)
+    return launch_kernel(skinny_kernel<2, true, false, false, false, false, EpiSplitUpdate>, pl.tiles * pl.splits, 512,
+                         0, s, A, lda, D, ldd, M, N, K, pl.chunk, e, CtxInput{});
   return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, pl.splits, pl.chunk, e);
-}
-
-hipError_t splitk_finish(hipStream_t s, int M, int N, int K, float* W, float* V, int ldw, float lr, float mom,
-                         const float* ws, float limit, unsigned long long* faults) {
-  const int sp = change_splits(M, N, K);
-  if (M <= 0 || N <= 0 || sp <= 1) return hipSuccess;
-  const int ldp = (N + 3) / 4 * 4;
-  const size_t total = (size_t)M * N;
-  return launch_kernel(splitk_update_kernel, (unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s, 
-      ws, sp, (size_t)M * ldp, M, N, ldp, W, V, ldw, lr, mom, limit, faults);
 }
 
 hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb, float lr,

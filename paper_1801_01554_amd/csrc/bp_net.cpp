@@ -43,6 +43,7 @@ struct bp_net {
   size_t fwd_cap = 0;
   float* splitk = nullptr;
   size_t splitk_cap = 0;
+  int* arrivals = nullptr;            // split-K arrival counters (bpk::kMaxArrivals), zero between launches
   double* sse_part = nullptr;
   size_t sse_cap = 0;
   double* sse_dev = nullptr;
@@ -382,14 +383,11 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
     }
     const float* A = (l == 0) ? in.x : net->act[l];
     const int ldA = (l == 0) ? ldx_of(net, in) : net->lda[l];
-    BP_LAUNCH(net, BP_K_CHANGE,
+    const bool split = bpk::change_splits(net->n[l], net->n[l + 1], rows) > 1;
+    BP_LAUNCH(net, split ? BP_K_SPLITK : BP_K_CHANGE,
               bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
-                                 wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk, net->fault_limit,
-                                 net->faults));
-    if (bpk::change_splits(net->n[l], net->n[l + 1], rows) > 1)
-      BP_LAUNCH(net, BP_K_SPLITK,
-                bpk::splitk_finish(s, net->n[l], net->n[l + 1], rows, wl(net, l), vl(net, l), net->ldw[l], lr, mom,
-                                   net->splitk, net->fault_limit, net->faults));
+                                 wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk, net->arrivals,
+                                 net->fault_limit, net->faults));
     BP_LAUNCH(net, BP_K_BIAS,
               bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1],
                                (l + 1 == net->L && top_csum > 0) ? top_csum : bpk::colsum_rows(rows), net->n[l + 1],
@@ -792,11 +790,14 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
   if (e == hipSuccess) e = hipMalloc(&net->V, sizeof(float) * net->wtotal);
   if (e == hipSuccess) e = hipMemset(net->W, 0, sizeof(float) * net->wtotal);
   if (e == hipSuccess) e = hipMemset(net->V, 0, sizeof(float) * net->wtotal);
+  if (e == hipSuccess) e = hipMalloc(&net->arrivals, sizeof(int) * bpk::kMaxArrivals);
+  if (e == hipSuccess) e = hipMemset(net->arrivals, 0, sizeof(int) * bpk::kMaxArrivals);
   if (e != hipSuccess) {
     hip_fail(nullptr, e, "bp_create");
     const int code = e == hipErrorOutOfMemory ? BP_ENOMEM : BP_EDEVICE;
     free_ptr(net->W);
     free_ptr(net->V);
+    free_ptr(net->arrivals);
     delete net;
     return code;
   }
@@ -821,6 +822,7 @@ void bp_destroy(bp_net* net) {
   free_ptr(net->seq_in);
   free_ptr(net->W);
   free_ptr(net->V);
+  free_ptr(net->arrivals);
   for (auto& r : net->recs) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
@@ -847,6 +849,9 @@ int bp_set_weights(bp_net* net, const float* w_host, int64_t n) {
   BP_HIP(net, hipStreamSynchronize(net->stream));
   BP_HIP(net, hipMemsetAsync(net->W, 0, sizeof(float) * net->wtotal, net->stream));
   BP_HIP(net, hipMemsetAsync(net->V, 0, sizeof(float) * net->wtotal, net->stream));
+  // the split-K arrival counters are zero between launches; clear them here too,
+  // in case a failed launch left some set
+  BP_HIP(net, hipMemsetAsync(net->arrivals, 0, sizeof(int) * bpk::kMaxArrivals, net->stream));
   return copy_layers(net, net->W, w_host, nullptr);
 }
 

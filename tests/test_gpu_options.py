@@ -126,7 +126,9 @@ POISON_CASES = [
     ((203, 120, 26), 64, 64, True, np.nan),        # fused small-net update
     ((203, 300, 26), 96, 96, True, 1e30),          # one-hot scatter + dense output change
     ((70, 45, 9), 200, 200, False, 1e30),          # dense change products (fused update epilogue)
-    ((40, 30, 20), 2048, 2048, False, np.nan),     # split-K change + bias rows
+    ((40, 30, 20), 2048, 2048, False, np.nan),     # split-K change (skinny kernel) + bias rows
+    ((1100, 1100, 4), 1030, 1030, False, np.nan),  # change split 4 ways over blocks (last block updates)
+    ((2000, 2100, 6), 1100, 1100, False, 1e30),    # change split 2 ways, ragged second split
     ((33, 20, 12, 5), 100, 100, False, 1e30),      # three layers
 ]
 

@@ -129,6 +129,10 @@ def test_first_update_full_size(dev, name):
     ((97, 33, 3), 2500, 2500, False),
     ((64, 200, 10), 4096, 4096, False),
     ((1, 40, 1), 1500, 1500, False),
+    # change products on 128 x 128 tiles split over blocks, the last block of each tile adding the
+    # splits and applying the update: 2 splits (the second ragged) and 8 splits
+    ((2000, 2100, 10), 1100, 1100, False),
+    ((800, 800, 3), 2100, 2100, False),
 ])
 def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
