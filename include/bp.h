@@ -114,6 +114,23 @@ int bp_get_momentum(const bp_net* net, float* v_host, int64_t n);
 int bp_train_batches(bp_net* net, const float* inputs_dev, const float* targets_dev, int64_t n_patterns,
                      int32_t batch, float lr, float momentum, double* sse_out);
 
+/* bp_train_batches for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): same arguments, same launches and the same results, bit for
+ * bit.  The call's workspace (activations, deltas, column sums, split-K
+ * partials and counters, error partials) lives in a fixed 64 MiB array per
+ * GPU, held by the library until the process ends, instead of in the net's
+ * own allocations; nothing is allocated or freed, and no graph is captured
+ * (every launch is issued directly).  The array is shared by every net and
+ * every call on that GPU and keeps the last call's contents: calls that
+ * overlap on one GPU (different streams, or host threads) race.  Returns
+ * BP_EINVAL, with a message giving the bytes needed, when the call's
+ * workspace exceeds 64 MiB (it grows with batch x the layer widths: batch
+ * 512 on a 512-2048-2048-2048-64 net needs about 26 MB, batch 1024 about
+ * 84 MB); otherwise as bp_train_batches. */
+int bp_train_batches_noalloc(bp_net* net, const float* inputs_dev, const float* targets_dev, int64_t n_patterns,
+                             int32_t batch, float lr, float momentum, double* sse_out);
+
 /* As bp_train_batches, for inputs that are 0/1 with exactly n_active ones per
  * pattern (the NETtalk window coding: 7 positions x 29 symbols, section 6.3),
  * given as the indices of the ones:

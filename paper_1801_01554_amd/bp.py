@@ -23,7 +23,8 @@ LIB_PATH = os.path.join(HERE, "libbp.so")
 
 BP_OK, BP_EINVAL, BP_ENOMEM, BP_EDEVICE = 0, -1, -2, -3
 EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set_weights", "bp_get_weights",
-           "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_onehot", "bp_forward",
+           "bp_set_momentum", "bp_get_momentum", "bp_train_batches", "bp_train_batches_noalloc",
+           "bp_train_batches_onehot", "bp_forward",
            "bp_forward_onehot", "bp_set_context", "bp_train_sequences", "bp_forward_sequences", "bp_set_sigmoid", "bp_set_fault_limit", "bp_get_fault_count",
            "bp_checkpoint_save", "bp_checkpoint_restore", "bp_guard_config", "bp_guard_epoch", "bp_set_graph_replay", "bp_profile",
            "bp_profile_report", "bp_last_error")
@@ -63,6 +64,8 @@ def lib():
         "bp_get_momentum": (ctypes.c_int, [_vp, _f32p, ctypes.c_int64]),
         "bp_train_batches": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
                                             ctypes.c_float, _f64p]),
+        "bp_train_batches_noalloc": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
+                                                    ctypes.c_float, _f64p]),
         "bp_train_batches_onehot": (ctypes.c_int, [_vp, _vp, ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int32,
                                                    ctypes.c_float, ctypes.c_float, _f64p]),
         "bp_forward": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, _vp]),
@@ -132,6 +135,12 @@ def bp_train_batches(h, inputs_ptr: int, targets_ptr: int, n: int, batch: int, l
                      sse: Optional[ctypes.c_double]) -> int:
     return lib().bp_train_batches(h, _vp(inputs_ptr), _vp(targets_ptr), n, batch, lr, momentum,
                                   ctypes.byref(sse) if sse is not None else None)
+
+
+def bp_train_batches_noalloc(h, inputs_ptr: int, targets_ptr: int, n: int, batch: int, lr: float, momentum: float,
+                             sse: Optional[ctypes.c_double]) -> int:
+    return lib().bp_train_batches_noalloc(h, _vp(inputs_ptr), _vp(targets_ptr), n, batch, lr, momentum,
+                                          ctypes.byref(sse) if sse is not None else None)
 
 
 def bp_train_batches_onehot(h, active_ptr: int, n_active: int, targets_ptr: int, n: int, batch: int, lr: float,

@@ -198,4 +198,7 @@ hipError_t seq_assemble(hipStream_t s, const float* X, int n_ext, const float* c
 // out[0] = sum of part[0 .. n-1] in a fixed order (double).
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out);
 
+// Sets p[0, n) to zero with a kernel (no memset node when captured).
+hipError_t zero_ints(hipStream_t s, int* p, int n);
+
 }  // namespace bpk

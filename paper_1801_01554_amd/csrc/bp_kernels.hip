@@ -1171,6 +1171,13 @@ __global__ __launch_bounds__(kThreads) void onehot_update_kernel(const int32_t* 
   if (limit > 0.f) add_faults(nf, faults);
 }
 
+// Zero fill of n ints (counters that must start at zero, in work a caller
+// may capture into a graph, where a memset node is avoided).
+__global__ __launch_bounds__(kThreads) void zero_ints_kernel(int* p, int n) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
 // Fixed-order sum of n doubles by one block of 1024 threads: thread t adds
 // elements t, t + 1024, ... (loads issued eight at a time), then a tree.
 constexpr int kRed = 1024;
@@ -1407,6 +1414,11 @@ hipError_t onehot_update(hipStream_t s, const int32_t* act, int n_active, int ro
 
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out) {
   return launch_kernel(sse_reduce_kernel, 1, kRed, 0, s, part, n, out);
+}
+
+hipError_t zero_ints(hipStream_t s, int* p, int n) {
+  if (n <= 0) return hipSuccess;
+  return launch_kernel(zero_ints_kernel, (n + kThreads - 1) / kThreads, kThreads, 0, s, p, n);
 }
 
 }  // namespace bpk

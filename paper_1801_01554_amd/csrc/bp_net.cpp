@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -111,7 +112,42 @@ struct bp_net {
   mutable std::string err;            // message of the last failure (read-only calls set it too)
 };
 
+// Workspace of bp_train_batches_noalloc, for callers that cannot allocate:
+// one array per GPU, held until the process ends.  Host code never uses the
+// array's name as an address (on the host it is a stand-in, not device
+// memory): bp_create looks up each device's copy once, with that device
+// current, and the entry point takes that address.  Every call on a GPU
+// shares the GPU's copy, so calls that overlap on one GPU race.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device` (which must be current on the
+// first call for it); nullptr on failure.
+float* scratch_on(int device, hipError_t* err) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  *err = hipSuccess;
+  if (device < 0 || device >= kMaxDevices) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess) return nullptr;
+    if (!p) {
+      *err = hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    g_scratch_ptr[device] = static_cast<float*>(p);
+  }
+  return g_scratch_ptr[device];
+}
 
 thread_local std::string g_create_err;
 
@@ -523,6 +559,90 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
   return BP_OK;
 }
 
+// A training call whose workspace is carved out of the device's `scratch`
+// instead of the net's allocations: the same launches as train(), issued
+// directly (no graph, no profiling events), with the net's workspace views
+// pointed into the scratch for the call and restored afterwards.
+int train_noalloc(bp_net* net, const BatchInput& in, const float* targets, int64_t n, int32_t batch, float lr,
+                  float mom, double* sse_out) {
+  if (n == 0) {
+    if (sse_out) *sse_out = 0.0;
+    return BP_OK;
+  }
+  hipError_t e = hipSuccess;
+  float* base = scratch_on(net->device, &e);
+  if (!base) return hip_fail(net, e, "bp_train_batches_noalloc: scratch address");
+  const int64_t rows_max = std::min<int64_t>(batch, n);
+  const int64_t nb = (n + batch - 1) / batch;
+  const int last_rows = (int)(n - (nb - 1) * (int64_t)batch);
+  const size_t sk = std::max(splitk_floats(net, rows_max, rows_max), splitk_floats(net, last_rows, last_rows));
+  const size_t n_sse = (size_t)sse_blocks(net, in, (int)rows_max) * (size_t)(nb - 1) +
+                       (size_t)sse_blocks(net, in, last_rows);
+  // layout, each piece on a 256-byte boundary: act[1..L-1], del[1..L],
+  // csum[1..L], split partials, arrival counters, error partials, error sum
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    const size_t o = off;
+    off += (floats + 63) / 64 * 64;
+    return o;
+  };
+  std::vector<size_t> oa(net->L + 1, 0), od(net->L + 1, 0), oc(net->L + 1, 0);
+  for (int l = 1; l <= net->L; ++l) {
+    if (l < net->L) oa[l] = take((size_t)rows_max * net->lda[l]);
+    od[l] = take((size_t)rows_max * net->lda[l]);
+    oc[l] = take((size_t)bpk::colsum_rows((int)rows_max) * net->lda[l]);
+  }
+  const size_t osk = take(sk);
+  const size_t oarr = take(bpk::kMaxArrivals);
+  const size_t osp = take(2 * n_sse);
+  const size_t osd = take(2);
+  if (off * sizeof(float) > kScratchBytes) {
+    char buf[256];
+    std::snprintf(buf, sizeof(buf),
+                  "bp_train_batches_noalloc: the call needs %zu bytes of workspace, more than the %zu-byte "
+                  "scratch (use a smaller batch, or bp_train_batches)",
+                  off * sizeof(float), kScratchBytes);
+    return fail(net, BP_EINVAL, buf);
+  }
+  // swap the views in, run, swap back
+  std::vector<float*> act = net->act, del = net->del, csum = net->csum;
+  float* splitk = net->splitk;
+  int* arrivals = net->arrivals;
+  double* sse_part = net->sse_part;
+  double* sse_dev = net->sse_dev;
+  const bool prof = net->prof;
+  for (int l = 1; l <= net->L; ++l) {
+    net->act[l] = l < net->L ? base + oa[l] : nullptr;
+    net->del[l] = base + od[l];
+    net->csum[l] = base + oc[l];
+  }
+  net->splitk = base + osk;
+  net->arrivals = reinterpret_cast<int*>(base + oarr);
+  net->sse_part = reinterpret_cast<double*>(base + osp);
+  net->sse_dev = reinterpret_cast<double*>(base + osd);
+  net->prof = false;
+  // the counters start at zero (every finished launch leaves them so; an
+  // earlier call that failed part way might not have)
+  const hipError_t ez = bpk::zero_ints(net->stream, net->arrivals, bpk::kMaxArrivals);
+  int rc = ez == hipSuccess ? BP_OK : hip_fail(net, ez, "bp_train_batches_noalloc: counter reset");
+  if (rc == BP_OK) rc = train_launches(net, in, targets, n, batch, lr, mom);
+  double* sum = net->sse_dev;
+  net->act = act;
+  net->del = del;
+  net->csum = csum;
+  net->splitk = splitk;
+  net->arrivals = arrivals;
+  net->sse_part = sse_part;
+  net->sse_dev = sse_dev;
+  net->prof = prof;
+  if (rc) return rc;
+  if (sse_out) {
+    BP_HIP(net, hipMemcpyAsync(sse_out, sum, sizeof(double), hipMemcpyDeviceToHost, net->stream));
+    BP_HIP(net, hipStreamSynchronize(net->stream));
+  }
+  return BP_OK;
+}
+
 // ---- Elman nets (section 10.5)
 
 // Activation rows of `step` (S rows each) in the window buffers, per hidden
@@ -792,6 +912,7 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
   if (e == hipSuccess) e = hipMemset(net->V, 0, sizeof(float) * net->wtotal);
   if (e == hipSuccess) e = hipMalloc(&net->arrivals, sizeof(int) * bpk::kMaxArrivals);
   if (e == hipSuccess) e = hipMemset(net->arrivals, 0, sizeof(int) * bpk::kMaxArrivals);
+  if (e == hipSuccess) (void)scratch_on(net->device, &e);   // this device's scratch address, once
   if (e != hipSuccess) {
     hip_fail(nullptr, e, "bp_create");
     const int code = e == hipErrorOutOfMemory ? BP_ENOMEM : BP_EDEVICE;
@@ -897,6 +1018,15 @@ int bp_train_batches(bp_net* net, const float* inputs_dev, const float* targets_
   BatchInput in;
   in.x = inputs_dev;
   return train(net, in, targets_dev, n_patterns, batch, lr, momentum, sse_out);
+}
+
+int bp_train_batches_noalloc(bp_net* net, const float* inputs_dev, const float* targets_dev, int64_t n_patterns,
+                             int32_t batch, float lr, float momentum, double* sse_out) {
+  int rc = check_train(net, inputs_dev, targets_dev, n_patterns, batch, "bp_train_batches_noalloc");
+  if (rc) return rc;
+  BatchInput in;
+  in.x = inputs_dev;
+  return train_noalloc(net, in, targets_dev, n_patterns, batch, lr, momentum, sse_out);
 }
 
 int bp_train_batches_onehot(bp_net* net, const int32_t* active_dev, int32_t n_active, const float* targets_dev,
