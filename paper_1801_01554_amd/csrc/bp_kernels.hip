@@ -584,11 +584,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
 
 // Tile configurations: 128 x 128 x 32 (wave tile 64 x 64, two blocks per
 // CU, 72 KB of LDS with both buffers) for products with at least one tile
-// per CU or deep enough in K for split-K to fill the chip; 64 x 64 x 32
-// (wave tile 32 x 32) for the other, small products, which gives them four
-// times the blocks (and wastes less of an edge tile).  (A 256 x
-// 128 x 16 tile, one block per CU round for more products, measured slower
-// on the wide and deep nets.)
+// per CU or deep enough in K for split-K to fill the chip, 128 x 64 among
+// those when N <= 64 (half of a 128-wide tile would be empty columns);
+// 64 x 64 x 32 (wave tile 32 x 32) for the other, small products, which
+// gives them four times the blocks (and wastes less of an edge tile).  (A
+// 256 x 128 x 16 tile, one block per CU round for more products, measured
+// slower on the wide and deep nets.)
 constexpr int kTileK = 32;
 constexpr int kChunkAlign = kTileK;   // split-K chunks are multiples of BK
 constexpr int kCUs = 256;
@@ -596,7 +597,15 @@ constexpr int kCUs = 256;
 inline int tiles_of(int M, int N, int t) { return ((M + t - 1) / t) * ((N + t - 1) / t); }
 // Edge of the square tile an M x N product summed over K uses.
 inline int tile_edge(int M, int N, int K) { return (tiles_of(M, N, 128) >= kCUs || K >= 1024) ? 128 : 64; }
-inline int tile_count(int M, int N, int K) { return tiles_of(M, N, tile_edge(M, N, K)); }
+// Column edge of that tile.
+inline int tile_cols(int M, int N, int K) {
+  const int t = tile_edge(M, N, K);
+  return t == 128 && N <= 64 ? 64 : t;
+}
+inline int tile_count(int M, int N, int K) {
+  const int bm = tile_edge(M, N, K), bn = tile_cols(M, N, K);
+  return ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+}
 
 template <int BM, int BN, int BK, bool A_KM, bool B_NK, class Epi>
 hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K,
@@ -622,8 +631,11 @@ hipError_t launch_gemm(hipStream_t s, const float* A, int lda, const float* B, i
 template <bool A_KM, bool B_NK, class Epi>
 hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, int ldb, int M, int N, int K, int splits,
                       int k_chunk, const Epi& epi) {
-  if (tile_edge(M, N, K) == 128)
+  if (tile_edge(M, N, K) == 128) {
+    if (tile_cols(M, N, K) == 64)
+      return launch_gemm<128, 64, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
     return launch_gemm<128, 128, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
+  }
   return launch_gemm<64, 64, kTileK, A_KM, B_NK>(s, A, lda, B, ldb, M, N, K, splits, k_chunk, epi);
 }
 
@@ -1348,8 +1360,7 @@ ChangePlan change_plan(int M, int N, int K) {
     if (sp >= 2) return {true, sp, chunk, tiles, 64 * 32};
   }
   const int sp = choose_splits(M, N, K);
-  const int t = tile_edge(M, N, K);
-  return {false, sp, sp > 1 ? chunk_for(K, sp) : K, tiles_of(M, N, t), t * t};
+  return {false, sp, sp > 1 ? chunk_for(K, sp) : K, tile_count(M, N, K), tile_edge(M, N, K) * tile_cols(M, N, K)};
 }
 
 int change_splits(int M, int N, int K) { return change_plan(M, N, K).splits; }
