@@ -512,6 +512,82 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       }
     if (epi.limit > 0.f) add_faults(nf, epi.faults);
   } else {
+    // Row epilogue of full 128 x 128 tiles for the sigmoid and hidden-delta
+    // products: the accumulators go to LDS (the idle stage buffers, rows 0-63
+    // in As and 64-127 in Bs, row stride 136 floats: the two lane halves of a
+    // register write land 32 banks apart), then each thread takes 4 adjacent
+    // columns of 16 rows (rows t / 32 + 8 i) as float4: one 16-byte load of
+    // the operand and one 16-byte store per row instead of four 4-byte ones,
+    // every wave instruction covering whole cache lines.
+    constexpr bool kRowEpi = (std::is_same_v<Epi, EpiSigmoid> || std::is_same_v<Epi, EpiHiddenDelta>) &&
+                             BM == 128 && BN == 128;
+    if constexpr (kRowEpi) {
+      constexpr int RS = 136;
+      static_assert(64 * RS <= 2 * T::A_ELEMS && 64 * RS <= 2 * T::B_ELEMS, "row epilogue fits the stage buffers");
+      bool vec = m0 + BM <= M && n0 + BN <= N && (epi.ldo & 3) == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0;
+      if constexpr (std::is_same_v<Epi, EpiHiddenDelta>)
+        vec = vec && (epi.lda & 3) == 0 && (reinterpret_cast<uintptr_t>(epi.act) & 15) == 0;
+      if (vec) {
+        float* lo = &As[0][0];
+        float* hi = &Bs[0][0];
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+          for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int row = wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), col = wn0 + j * 32 + r;
+              (row < 64 ? lo : hi)[(row & 63) * RS + col] = acc[i][j][e];
+            }
+        __syncthreads();
+        const int c4 = tid & 31, r0 = tid >> 5;
+        const int n = n0 + 4 * c4;
+        f32x4 cs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+        f32x4 b4 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (std::is_same_v<Epi, EpiSigmoid>)
+          b4 = f32x4{epi.bias[n], epi.bias[n + 1], epi.bias[n + 2], epi.bias[n + 3]};
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          f32x4 pre[8];
+          if constexpr (std::is_same_v<Epi, EpiHiddenDelta>) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              pre[i] = *reinterpret_cast<const f32x4*>(epi.act + (size_t)(m0 + 64 * g + r0 + 8 * i) * epi.lda + n);
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int row = r0 + 8 * i;
+            const f32x4 a = *reinterpret_cast<const f32x4*>((g ? hi : lo) + row * RS + 4 * c4);
+            f32x4 v;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if constexpr (std::is_same_v<Epi, EpiSigmoid>)
+                v[q] = unit_sigma(a[q] + b4[q], epi.tab);
+              else
+                v[q] = a[q] * (pre[i][q] * (1.0f - pre[i][q]));
+            }
+            *reinterpret_cast<f32x4*>(epi.out + (size_t)(m0 + 64 * g + row) * epi.ldo + n) = v;
+            if constexpr (Epi::kColSum) cs[g] += v;
+          }
+        }
+        if constexpr (Epi::kColSum) {
+          // per 64-row group: the 8 row slices (r0) of each column added in
+          // slice order
+          __syncthreads();
+          f32x4* red = reinterpret_cast<f32x4*>(lo);          // [2][8][32] float4
+#pragma unroll
+          for (int g = 0; g < 2; ++g) red[(g * 8 + r0) * 32 + c4] = cs[g];
+          __syncthreads();
+          if (tid < 64) {
+            const int g = tid >> 5, cc = tid & 31;
+            f32x4 t = red[(g * 8) * 32 + cc];
+            for (int k = 1; k < 8; ++k) t += red[(g * 8 + k) * 32 + cc];
+            *reinterpret_cast<f32x4*>(epi.colsum + (size_t)(tm * 2 + g) * epi.ldcs + n0 + 4 * cc) = t;
+          }
+        }
+        return;
+      }
+    }
     float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
     // The per-element operands of each 32 x 32 block are loaded together
     // (clamped, always valid addresses; values outside the matrix are never
