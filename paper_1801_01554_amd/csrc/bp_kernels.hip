@@ -260,30 +260,32 @@ __device__ __forceinline__ void ordered_split_sum(f32x4 (&g)[NS], const f32x4 (&
 // t (t = 0..3) pairs k = 8g + t (lanes 0-31) with k = 8g + 4 + t (lanes
 // 32-63); A and B use the same assignment, so each lane can fetch its four k
 // values of a k-contiguous tile with one 16-byte LDS read.
-template <int BM, int BN, int BK, bool A_KM, bool B_NK>
+template <int BM, int BN, int BK, bool A_KM, bool B_NK, int NTH = kThreads>
 struct Tile {
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  // wave grid: 2 x 2 waves for 256 threads, 2 x 4 for 512 (wave tile 128 x 64)
+  static constexpr int WGM = 2, WGN = NTH / 128;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int SA = A_KM ? (BM + 8) : (BK + 4);   // LDS row strides (floats)
   static constexpr int SB = B_NK ? (BK + 4) : (BN + 8);
   static constexpr int A_ELEMS = A_KM ? BK * SA : BM * SA;
   static constexpr int B_ELEMS = B_NK ? BN * SB : BK * SB;
-  static constexpr int LA = BM * BK / 4 / kThreads;        // float4 loads per thread per stage
-  static constexpr int LB = BN * BK / 4 / kThreads;
+  static constexpr int LA = BM * BK / 4 / NTH;             // float4 loads per thread per stage
+  static constexpr int LB = BN * BK / 4 / NTH;
   static_assert(BM % 64 == 0 && BN % 64 == 0 && BK % 8 == 0, "tile shape");
-  static_assert(LA * 4 * kThreads == BM * BK && LB * 4 * kThreads == BN * BK, "tile split");
+  static_assert(LA * 4 * NTH == BM * BK && LB * 4 * NTH == BN * BK, "tile split");
 };
 
 // Loads a TO x TD tile (TD contiguous) whose origin is (o0, d0) into
 // registers; elements outside [0, O_lim) x [0, D_lim) read as zero.
-template <int TO, int TD, bool VEC>
+template <int TO, int TD, bool VEC, int NTH = kThreads>
 __device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld, int o0, int d0, int O_lim,
                                           int D_lim, f32x4* r, int tid) {
-  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int PER = TO * TD / 4 / NTH;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = tid + q * kThreads;
+    const int f = tid + q * NTH;
     const int go = o0 + f / D4, gd = d0 + (f % D4) * 4;
     f32x4 v = {0.f, 0.f, 0.f, 0.f};
     if (go < O_lim) {
@@ -302,25 +304,25 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ base, int ld
 
 // Loads a TO x TD tile that lies entirely inside the matrix, 16 bytes per
 // load, with no bounds checks (interior tiles of 16-byte aligned operands).
-template <int TO, int TD>
+template <int TO, int TD, int NTH = kThreads>
 __device__ __forceinline__ void load_tile_full(const float* __restrict__ base, int ld, int o0, int d0, f32x4* r,
                                                int tid) {
-  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int PER = TO * TD / 4 / NTH;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = tid + q * kThreads;
+    const int f = tid + q * NTH;
     r[q] = *reinterpret_cast<const f32x4*>(base + (size_t)(o0 + f / D4) * ld + d0 + (f % D4) * 4);
   }
 }
 
-template <int TO, int TD, int S>
+template <int TO, int TD, int S, int NTH = kThreads>
 __device__ __forceinline__ void store_tile(float* lds, const f32x4* r, int tid) {
-  constexpr int PER = TO * TD / 4 / kThreads;
+  constexpr int PER = TO * TD / 4 / NTH;
   constexpr int D4 = TD / 4;
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int f = tid + q * kThreads;
+    const int f = tid + q * NTH;
     *reinterpret_cast<f32x4*>(lds + (f / D4) * S + (f % D4) * 4) = r[q];
   }
 }
@@ -342,11 +344,16 @@ __device__ __forceinline__ void xcd_tile(int bid, int nblocks, int tiles_m, int 
   tn = in_band / rows;
 }
 
-template <int BM, int BN, int BK, bool A_KM, bool B_NK, bool AVEC, bool BVEC, class Epi>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict__ A, int lda,
-                                                        const float* __restrict__ B, int ldb, int M, int N,
-                                                        int K, int k_chunk, Epi epi) {
-  using T = Tile<BM, BN, BK, A_KM, B_NK>;
+template <int BM, int BN, int BK, bool A_KM, bool B_NK, bool AVEC, bool BVEC, class Epi, int NTH = kThreads>
+__global__ __launch_bounds__(NTH) void gemm_kernel(const float* __restrict__ A, int lda,
+                                                   const float* __restrict__ B, int ldb, int M, int N,
+                                                   int K, int k_chunk, Epi epi) {
+  using T = Tile<BM, BN, BK, A_KM, B_NK, NTH>;
+  // 512-thread blocks (256 x 256 tiles) only for full tiles of the sigmoid and
+  // hidden-delta products, which end through the row epilogue
+  static_assert(NTH == kThreads || ((std::is_same_v<Epi, EpiSigmoid> || std::is_same_v<Epi, EpiHiddenDelta>) &&
+                                    BM == 256 && BN == 256),
+                "512-thread tiles: full-tile sigmoid and hidden-delta products");
   __shared__ __attribute__((aligned(16))) float As[2][T::A_ELEMS];
   __shared__ __attribute__((aligned(16))) float Bs[2][T::B_ELEMS];
 
@@ -359,7 +366,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   const int ke = min(K, kb + k_chunk);
 
   const int wave = tid >> 6, lane = tid & 63;
-  const int wm0 = (wave >> 1) * T::WM, wn0 = (wave & 1) * T::WN;
+  const int wm0 = (wave / T::WGN) * T::WM, wn0 = (wave % T::WGN) * T::WN;
   const int r = lane & 31, h = lane >> 5;
 
   f32x16 acc[T::TM][T::TN];
@@ -377,27 +384,34 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
   // Interior tiles (the block-uniform common case) take the unchecked path.
   const bool a_rows_in = m0 + BM <= M, b_rows_in = n0 + BN <= N;
   auto load_stage = [&](int k, f32x4* ra, f32x4* rb) {
+    if constexpr (NTH != kThreads) {   // launched only on whole tiles: M, N, K multiples of the tile
+      if (A_KM) load_tile_full<BK, BM, NTH>(A, lda, k, m0, ra, tid);
+      else load_tile_full<BM, BK, NTH>(A, lda, m0, k, ra, tid);
+      if (B_NK) load_tile_full<BN, BK, NTH>(B, ldb, n0, k, rb, tid);
+      else load_tile_full<BK, BN, NTH>(B, ldb, k, n0, rb, tid);
+      return;
+    }
     const bool k_in = k + BK <= ke;
     if (AVEC && a_rows_in && k_in) {
-      if (A_KM) load_tile_full<BK, BM>(A, lda, k, m0, ra, tid);
-      else load_tile_full<BM, BK>(A, lda, m0, k, ra, tid);
+      if (A_KM) load_tile_full<BK, BM, NTH>(A, lda, k, m0, ra, tid);
+      else load_tile_full<BM, BK, NTH>(A, lda, m0, k, ra, tid);
     } else {
-      if (A_KM) load_tile<BK, BM, AVEC>(A, lda, k, m0, ke, M, ra, tid);
-      else load_tile<BM, BK, AVEC>(A, lda, m0, k, M, ke, ra, tid);
+      if (A_KM) load_tile<BK, BM, AVEC, NTH>(A, lda, k, m0, ke, M, ra, tid);
+      else load_tile<BM, BK, AVEC, NTH>(A, lda, m0, k, M, ke, ra, tid);
     }
     if (BVEC && b_rows_in && k_in) {
-      if (B_NK) load_tile_full<BN, BK>(B, ldb, n0, k, rb, tid);
-      else load_tile_full<BK, BN>(B, ldb, k, n0, rb, tid);
+      if (B_NK) load_tile_full<BN, BK, NTH>(B, ldb, n0, k, rb, tid);
+      else load_tile_full<BK, BN, NTH>(B, ldb, k, n0, rb, tid);
     } else {
-      if (B_NK) load_tile<BN, BK, BVEC>(B, ldb, n0, k, N, ke, rb, tid);
-      else load_tile<BK, BN, BVEC>(B, ldb, k, n0, ke, N, rb, tid);
+      if (B_NK) load_tile<BN, BK, BVEC, NTH>(B, ldb, n0, k, N, ke, rb, tid);
+      else load_tile<BK, BN, BVEC, NTH>(B, ldb, k, n0, ke, N, rb, tid);
     }
   };
   auto store_stage = [&](int buf, const f32x4* ra, const f32x4* rb) {
-    if (A_KM) store_tile<BK, BM, T::SA>(As[buf], ra, tid);
-    else store_tile<BM, BK, T::SA>(As[buf], ra, tid);
-    if (B_NK) store_tile<BN, BK, T::SB>(Bs[buf], rb, tid);
-    else store_tile<BK, BN, T::SB>(Bs[buf], rb, tid);
+    if (A_KM) store_tile<BK, BM, T::SA, NTH>(As[buf], ra, tid);
+    else store_tile<BM, BK, T::SA, NTH>(As[buf], ra, tid);
+    if (B_NK) store_tile<BN, BK, T::SB, NTH>(Bs[buf], rb, tid);
+    else store_tile<BK, BN, T::SB, NTH>(Bs[buf], rb, tid);
   };
   auto compute = [&](int buf) {
     const float* as = As[buf];
@@ -444,18 +458,36 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
     if (s + 1 < nst) store_stage((s + 1) & 1, rsa, rsb);
     __syncthreads();
   };
-  if (nst > 0) {
-    load_stage(kb, ra0, rb0);
-    if (nst > 1) load_stage(kb + BK, ra1, rb1);
-    store_stage(0, ra0, rb0);
-    __syncthreads();
+  if constexpr (NTH != kThreads) {
+    // 512-thread blocks hold twice the accumulators per wave; one register
+    // set suffices there, as a stage is twice the MFMA work per SIMD (two
+    // waves of 128 x 64 each): the load of stage s + 1 lands while stage s
+    // is multiplied.
+    if (nst > 0) {
+      load_stage(kb, ra0, rb0);
+      store_stage(0, ra0, rb0);
+      __syncthreads();
+    }
+    for (int s = 0; s < nst; ++s) {
+      if (s + 1 < nst) load_stage(kb + (s + 1) * BK, ra0, rb0);
+      compute(s & 1);
+      if (s + 1 < nst) store_stage((s + 1) & 1, ra0, rb0);
+      __syncthreads();
+    }
+  } else {
+    if (nst > 0) {
+      load_stage(kb, ra0, rb0);
+      if (nst > 1) load_stage(kb + BK, ra1, rb1);
+      store_stage(0, ra0, rb0);
+      __syncthreads();
+    }
+    int s = 0;
+    for (; s + 1 < nst; s += 2) {
+      step(s, ra0, rb0, ra1, rb1);       // even stage: loads s + 2 into set 0, stores set 1 (stage s + 1)
+      step(s + 1, ra1, rb1, ra0, rb0);   // odd stage: loads s + 3 into set 1, stores set 0 (stage s + 2)
+    }
+    if (s < nst) step(s, ra0, rb0, ra1, rb1);
   }
-  int s = 0;
-  for (; s + 1 < nst; s += 2) {
-    step(s, ra0, rb0, ra1, rb1);       // even stage: loads s + 2 into set 0, stores set 1 (stage s + 1)
-    step(s + 1, ra1, rb1, ra0, rb0);   // odd stage: loads s + 3 into set 1, stores set 0 (stage s + 2)
-  }
-  if (s < nst) step(s, ra0, rb0, ra1, rb1);
 
   // Accumulator layout of a 32 x 32 block: register e of lane (h, r) holds
   // row 8 (e / 4) + 4 h + (e % 4), column r.
@@ -512,82 +544,96 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
       }
     if (epi.limit > 0.f) add_faults(nf, epi.faults);
   } else {
-    // Row epilogue of full 128 x 128 tiles for the sigmoid and hidden-delta
-    // products: the accumulators go to LDS (the idle stage buffers, rows 0-63
-    // in As and 64-127 in Bs, row stride 136 floats: the two lane halves of a
-    // register write land 32 banks apart), then each thread takes 4 adjacent
-    // columns of 16 rows (rows t / 32 + 8 i) as float4: one 16-byte load of
-    // the operand and one 16-byte store per row instead of four 4-byte ones,
-    // every wave instruction covering whole cache lines.
+    // Row epilogue of full 128 x 128 and 256 x 256 tiles for the sigmoid and
+    // hidden-delta products, 128 rows at a time: the accumulators of those
+    // rows go to LDS (the idle stage buffers, rows 0-63 in As and 64-127 in
+    // Bs, row stride BN + 8 floats: the two lane halves of a register write
+    // land 32 banks apart), then each thread takes 4 adjacent columns of 16
+    // rows (rows t / (BN / 4) + 8 i) as float4: one 16-byte load of the
+    // operand and one 16-byte store per row instead of four 4-byte ones, every
+    // wave instruction covering whole cache lines.
     constexpr bool kRowEpi = (std::is_same_v<Epi, EpiSigmoid> || std::is_same_v<Epi, EpiHiddenDelta>) &&
-                             BM == 128 && BN == 128;
+                             ((BM == 128 && BN == 128) || (BM == 256 && BN == 256));
     if constexpr (kRowEpi) {
-      constexpr int RS = 136;
-      static_assert(64 * RS <= 2 * T::A_ELEMS && 64 * RS <= 2 * T::B_ELEMS, "row epilogue fits the stage buffers");
+      constexpr int RS = BN + 8, C4N = BN / 4, SL = NTH / C4N;   // row stride; float4 per row; row slices
+      static_assert(SL == 8 && 64 * RS <= 2 * T::A_ELEMS && 64 * RS <= 2 * T::B_ELEMS,
+                    "row epilogue fits the stage buffers");
       bool vec = m0 + BM <= M && n0 + BN <= N && (epi.ldo & 3) == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0;
       if constexpr (std::is_same_v<Epi, EpiHiddenDelta>)
         vec = vec && (epi.lda & 3) == 0 && (reinterpret_cast<uintptr_t>(epi.act) & 15) == 0;
-      if (vec) {
+      if (NTH != kThreads || vec) {
         float* lo = &As[0][0];
         float* hi = &Bs[0][0];
-#pragma unroll
-        for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < T::TN; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int row = wm0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3), col = wn0 + j * 32 + r;
-              (row < 64 ? lo : hi)[(row & 63) * RS + col] = acc[i][j][e];
-            }
-        __syncthreads();
-        const int c4 = tid & 31, r0 = tid >> 5;
+        const int c4 = tid % C4N, r0 = tid / C4N;
         const int n = n0 + 4 * c4;
-        f32x4 cs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
         f32x4 b4 = {0.f, 0.f, 0.f, 0.f};
         if constexpr (std::is_same_v<Epi, EpiSigmoid>)
           b4 = f32x4{epi.bias[n], epi.bias[n + 1], epi.bias[n + 2], epi.bias[n + 3]};
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
-          f32x4 pre[8];
-          if constexpr (std::is_same_v<Epi, EpiHiddenDelta>) {
+        for (int hf = 0; hf < BM / 128; ++hf) {
+          if (hf > 0) __syncthreads();                     // the previous half is read
+          // a wave's rows lie in one half (WM <= 128); rb is their first row
+          // within it, a multiple of 64, so the buffer of each 32-row block
+          // is wave-uniform
+          const int rb = wm0 - 128 * hf;
+          if (rb >= 0 && rb < 128) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-              pre[i] = *reinterpret_cast<const f32x4*>(epi.act + (size_t)(m0 + 64 * g + r0 + 8 * i) * epi.lda + n);
-          }
+            for (int i = 0; i < T::TM; ++i) {
+              float* dst = (rb + i * 32 < 64 ? lo : hi) + ((rb + i * 32) & 63) * RS + wn0 + r;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int row = r0 + 8 * i;
-            const f32x4 a = *reinterpret_cast<const f32x4*>((g ? hi : lo) + row * RS + 4 * c4);
-            f32x4 v;
+              for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if constexpr (std::is_same_v<Epi, EpiSigmoid>)
-                v[q] = unit_sigma(a[q] + b4[q], epi.tab);
-              else
-                v[q] = a[q] * (pre[i][q] * (1.0f - pre[i][q]));
+                for (int e = 0; e < 16; ++e) dst[(8 * (e >> 2) + 4 * h + (e & 3)) * RS + j * 32] = acc[i][j][e];
             }
-            *reinterpret_cast<f32x4*>(epi.out + (size_t)(m0 + 64 * g + row) * epi.ldo + n) = v;
-            if constexpr (Epi::kColSum) cs[g] += v;
           }
-        }
-        if constexpr (Epi::kColSum) {
-          // per 64-row group: the 8 row slices (r0) of each column added in
-          // slice order
           __syncthreads();
-          f32x4* red = reinterpret_cast<f32x4*>(lo);          // [2][8][32] float4
+          f32x4 cs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-          for (int g = 0; g < 2; ++g) red[(g * 8 + r0) * 32 + c4] = cs[g];
-          __syncthreads();
-          if (tid < 64) {
-            const int g = tid >> 5, cc = tid & 31;
-            f32x4 t = red[(g * 8) * 32 + cc];
-            for (int k = 1; k < 8; ++k) t += red[(g * 8 + k) * 32 + cc];
-            *reinterpret_cast<f32x4*>(epi.colsum + (size_t)(tm * 2 + g) * epi.ldcs + n0 + 4 * cc) = t;
+          for (int g = 0; g < 2; ++g) {
+            const int mg = m0 + 128 * hf + 64 * g;
+            f32x4 pre[8];
+            if constexpr (std::is_same_v<Epi, EpiHiddenDelta>) {
+#pragma unroll
+              for (int i = 0; i < 8; ++i)
+                pre[i] = *reinterpret_cast<const f32x4*>(epi.act + (size_t)(mg + r0 + 8 * i) * epi.lda + n);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              const int row = r0 + 8 * i;
+              const f32x4 a = *reinterpret_cast<const f32x4*>((g ? hi : lo) + row * RS + 4 * c4);
+              f32x4 v;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                if constexpr (std::is_same_v<Epi, EpiSigmoid>)
+                  v[q] = unit_sigma(a[q] + b4[q], epi.tab);
+                else
+                  v[q] = a[q] * (pre[i][q] * (1.0f - pre[i][q]));
+              }
+              *reinterpret_cast<f32x4*>(epi.out + (size_t)(mg + row) * epi.ldo + n) = v;
+              if constexpr (Epi::kColSum) cs[g] += v;
+            }
+          }
+          if constexpr (Epi::kColSum) {
+            // per 64-row group: the 8 row slices (r0) of each column added in
+            // slice order
+            __syncthreads();
+            f32x4* red = reinterpret_cast<f32x4*>(lo);        // [2][8][C4N] float4
+#pragma unroll
+            for (int g = 0; g < 2; ++g) red[(g * 8 + r0) * C4N + c4] = cs[g];
+            __syncthreads();
+            if (tid < 2 * C4N) {
+              const int g = tid / C4N, cc = tid % C4N;
+              f32x4 t = red[(g * 8) * C4N + cc];
+              for (int k = 1; k < 8; ++k) t += red[(g * 8 + k) * C4N + cc];
+              *reinterpret_cast<f32x4*>(epi.colsum + (size_t)(tm * (BM / 64) + 2 * hf + g) * epi.ldcs + n0 + 4 * cc) =
+                  t;
+            }
           }
         }
         return;
       }
     }
+    if constexpr (NTH == kThreads) {
     float sse = 0.f;   // the epilogue's per-lane statistic (error, or fault count: exact below 2^24)
     // The per-element operands of each 32 x 32 block are loaded together
     // (clamped, always valid addresses; values outside the matrix are never
@@ -654,6 +700,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const float* __restrict_
         for (int w = 0; w < kThreads / 64; ++w) s += (double)red[w];
         epi.sse_part[blockIdx.x] = s;
       }
+    }
     }
   }
 }
@@ -746,6 +793,15 @@ hipError_t launch_cfg(hipStream_t s, const float* A, int lda, const float* B, in
 // rows they built to `out` (zeros in [K, ldo)), which the window's change
 // product reads.
 constexpr int kSkinnyChunk = 16;   // MFMA steps per load round
+
+// 256 x 256 tiles of 512 threads (one block per CU) for products made of at
+// least one full such tile per CU: one round of blocks instead of two rounds
+// of 128 x 128 tiles, so one prologue and one epilogue per CU and no second
+// round starting behind the first round's slowest blocks.
+inline bool big_tiles(int M, int N, int K) {
+  return M % 256 == 0 && N % 256 == 0 && K % kTileK == 0 && K > 0 && tiles_of(M, N, 256) >= kCUs;
+}
+inline bool vec16(const void* p, int ld) { return (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 inline bool use_skinny(int M, int N, int K) { return K <= 2048 && tiles_of(M, N, 64) < 128; }
 
@@ -1322,6 +1378,9 @@ hipError_t forward_layer(hipStream_t s, const float* A, int lda, const float* W,
                          const float* bias, float* out, int ldo, const float* tab) {
   EpiSigmoid e{bias, out, ldo, tab};
   if (use_skinny(M, N, K)) return launch_skinny<1, false>(s, A, lda, W, ldw, M, N, K, e);
+  if (big_tiles(M, N, K) && vec16(A, lda) && vec16(W, ldw) && vec16(out, ldo))
+    return launch_kernel(gemm_kernel<256, 256, kTileK, false, false, true, true, EpiSigmoid, 2 * kThreads>,
+                         tiles_of(M, N, 256), 2 * kThreads, 0, s, A, lda, W, ldw, M, N, K, K, e);
   return launch_cfg<false, false>(s, A, lda, W, ldw, M, N, K, 1, K, e);
 }
 
@@ -1408,6 +1467,9 @@ hipError_t backward_layer(hipStream_t s, const float* D, int ldd, const float* W
                           const float* act, int lda, float* out, int ldo, float* colsum, int ldcs) {
   EpiHiddenDelta e{act, lda, out, ldo, colsum, ldcs};
   if (use_skinny(M, N, K)) return launch_skinny<2, true>(s, D, ldd, W, ldw, M, N, K, e);
+  if (big_tiles(M, N, K) && vec16(D, ldd) && vec16(W, ldw) && vec16(out, ldo) && vec16(act, lda))
+    return launch_kernel(gemm_kernel<256, 256, kTileK, false, true, true, true, EpiHiddenDelta, 2 * kThreads>,
+                         tiles_of(M, N, 256), 2 * kThreads, 0, s, D, ldd, W, ldw, M, N, K, K, e);
   return launch_cfg<false, true>(s, D, ldd, W, ldw, M, N, K, 1, K, e);
 }
 

@@ -80,7 +80,7 @@ def _check_update(w, dev, batch, lr, mom, n=None, what=""):
 # --------------------------------------------------------------------------- forward
 @pytest.mark.parametrize("sizes,n", [((203, 80, 26), 1000), ((130, 257, 67), 300), ((1, 1), 5), ((64, 1), 129),
                                      ((1024, 4096, 1024), 512), ((512, 2048, 2048, 2048, 64), 256),
-                                     ((33, 5, 7, 9, 2), 40)])
+                                     ((33, 5, 7, 9, 2), 40), ((64, 4096, 256, 2048, 8), 4096)])
 def test_forward_matches_oracle(dev, sizes, n):
     w = wl.make_custom(sizes, n, seed=sum(sizes) + n, input_kind="normal")
     _say(f"case forward sizes={sizes} n={n}")
@@ -133,6 +133,10 @@ def test_first_update_full_size(dev, name):
     # splits and applying the update: 2 splits (the second ragged) and 8 splits
     ((2000, 2100, 10), 1100, 1100, False),
     ((800, 800, 3), 2100, 2100, False),
+    # sigmoid and hidden-delta products of 256 one-block 256 x 256 tiles (4096 x 4096 outputs, K a
+    # multiple of 32), and the same outputs with K = 40 and 100, which stay on 128 x 128 tiles
+    ((96, 4096, 32), 4096, 4096, False),
+    ((100, 4096, 40), 4096, 4096, False),
 ])
 def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
