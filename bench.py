@@ -50,7 +50,7 @@ PRIMARY = "deep-512-2048x3-64"
 SECONDARY = ("wide-1024-4096-1024", "nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16")
 VARIANT_WORKLOAD = "nettalk-120-b512"
 SECONDARY_SEQ = ("elman-64+256-256-64",)
-GEMM_KINDS = ("forward", "output", "backward", "change", "splitk", "seq_pair")
+GEMM_KINDS = ("forward", "output", "backward", "change", "splitk", "seq_pair", "seq_win")
 KERNEL_NAMES = {
     "forward": "gemm_kernel|skinny_kernel<..., EpiSigmoid>",
     "output": "gemm_kernel|skinny_kernel<..., EpiOutputDelta>",
@@ -66,6 +66,7 @@ KERNEL_NAMES = {
     "output_finish": "output_finish_kernel",
     "seq_in": "seq_assemble_kernel",
     "seq_pair": "elman_pair_kernel",
+    "seq_win": "elman_window_kernel",
 }
 SMALL_MAX_HIDDEN, SMALL_MAX_OUT, SMALL_MAX_ACTIVE = 256, 64, 32   # the library's fused-path limits
 
@@ -115,14 +116,26 @@ def kind_work(sizes, rows, onehot, n_active, splits_of, parts=("fwd", "bwd")):
     return w
 
 
-def seq_kind_work(sizes, n_ctx, S, steps, splits_of, built_steps=0, paired=False):
+def seq_kind_work(sizes, n_ctx, S, steps, splits_of, built_steps=0, paired=False, window=False):
     """Algorithmic (flops, HBM bytes) per kind of one Elman window: `steps` forward steps of S
     patterns, then one backward pass and update over steps x S rows.  `built_steps` of the steps
     have their input rows built by the first product (reading the flags besides X and the context
     source, writing the rows); the others assemble them first (seq_in).  `paired`: steps 1 ..
     steps - 1 run their hidden layer in one launch with the output layer of the step before
-    (seq_pair); the first step's hidden layer and the last step's output layer run alone."""
+    (seq_pair); the first step's hidden layer and the last step's output layer run alone.
+    `window`: the whole forward pass of the window is one launch (seq_win), which reads X, the
+    flags, the targets and the weights and writes the input rows, hidden units and output deltas."""
     n_ext = sizes[0] - n_ctx
+    if window:
+        n0, n1, n2 = sizes
+        step = kind_work(sizes, S, False, 0, splits_of, ("fwd",))
+        flops = steps * sum(f for f, _ in step.values())
+        io = 4.0 * S * (n_ext + 2 + n2 + n0 + n1 + n2)
+        w = {"seq_win": (flops, steps * io + 4.0 * ((n0 + 1) * n1 + (n1 + 1) * n2))}
+        for k, (f, b) in kind_work(sizes, steps * S, False, 0, splits_of, ("bwd",)).items():
+            f0, b0 = w.get(k, (0.0, 0.0))
+            w[k] = (f0 + f, b0 + b)
+        return w
     rows_bytes = 4.0 * S * (1 + -(-sizes[0] // 4) * 4)          # flags read, rows written
     w = {"seq_in": (0.0, (steps - built_steps) * (4.0 * S * (n_ext + n_ctx) + rows_bytes))}
 
@@ -169,6 +182,17 @@ def elman_pair(sizes, n_ctx, S):
     output layer of the step before (one hidden layer, both products on the skinny kernel)."""
     return (len(sizes) == 3 and input_built_in_product(sizes, n_ctx, S) and sizes[1] <= 2048
             and -(-S // 64) * -(-sizes[2] // 64) < 128)
+
+
+def elman_window(sizes, n_ctx, S):
+    """Mirror of the library's choice to run an Elman window's forward pass in one launch (one
+    hidden layer whose context copies it in order; sizes within the kernel's limits)."""
+    if len(sizes) != 3:
+        return False
+    n0, n1, n2 = sizes
+    n_ext = n0 - n_ctx
+    return (S > 0 and 0 < n_ctx <= n1 and n_ext >= 0 and n0 <= 512 and n1 <= 256 and n2 <= 256
+            and 4 * n_ext <= 1024 and 4 * n2 <= 1024)
 
 
 def change_splits(M, N, K):
@@ -374,9 +398,10 @@ def run_seq_workload(name, epochs, torch, bp, wl, metrics, log):
     for w0 in range(0, spec.n_steps, spec.steps_per_update):
         steps = min(spec.steps_per_update, spec.n_steps - w0)
         nb = (steps - 1 if w0 == 0 else steps) if built else 0     # one call per epoch: its first step assembles
-        paired = built and elman_pair(w.sizes, spec.n_ctx, spec.n_streams)
+        window = elman_window(w.sizes, spec.n_ctx, spec.n_streams)
+        paired = not window and built and elman_pair(w.sizes, spec.n_ctx, spec.n_streams)
         for k, (f, b) in seq_kind_work(w.sizes, spec.n_ctx, spec.n_streams, steps, change_splits, nb,
-                                       paired).items():
+                                       paired, window).items():
             f0, b0 = work.get(k, (0.0, 0.0))
             work[k] = (f0 + epochs * f, b0 + epochs * b)
     kernels, roof, gemm_f, gemm_ms = summarize_kernels(rep, work, name)

@@ -267,7 +267,8 @@ enum {
   BP_K_OUTFIN = 11,   /* split-K output layer: partial sums + deltas + error */
   BP_K_SEQ_IN = 12,   /* Elman nets: input rows of a step with the context copy */
   BP_K_SEQ_PAIR = 13, /* Elman nets: hidden layer of a step + output layer of the step before */
-  BP_K_COUNT = 14
+  BP_K_SEQ_WIN = 14,  /* Elman nets, one hidden layer: forward pass + output deltas of a window */
+  BP_K_COUNT = 15
 };
 
 /* Graph replay of repeated training calls (on by default).  With on != 0,

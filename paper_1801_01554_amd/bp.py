@@ -30,7 +30,7 @@ EXPORTS = ("bp_create", "bp_destroy", "bp_set_stream", "bp_num_weights", "bp_set
            "bp_profile_report", "bp_last_error")
 BP_SIGMOID_EXACT, BP_SIGMOID_TABLE = 0, 1
 KINDS = ("forward", "output", "backward", "change", "splitk", "bias", "gather", "scatter", "reduce", "fused_fb",
-         "fused_update", "output_finish", "seq_in", "seq_pair")
+         "fused_update", "output_finish", "seq_in", "seq_pair", "seq_win")
 
 _lib = None
 _vp = ctypes.c_void_p

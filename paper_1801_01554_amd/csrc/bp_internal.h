@@ -195,6 +195,50 @@ hipError_t seq_assemble(hipStream_t s, const float* X, int n_ext, const float* c
                         const int32_t* ctx_layer, const int32_t* ctx_unit, const CtxSource& src, float* A0,
                         int lda0);
 
+// The forward pass of one window of an Elman net with one hidden layer whose
+// context copies the hidden units in order (section 10.5), all steps in one
+// launch.  Streams are independent, so each block keeps the recurrence of
+// its own streams: step k's input rows (X, then cont x the hidden units of
+// step k - 1 of the same stream; step 0 takes them from Hprev, or zero),
+// hidden units, output units and output deltas, with no exchange between
+// blocks.  Step k of the window is rows k * S .. k * S + S - 1 of H, rows, D
+// (and of X, cont, mask, T, each given at the window's first step).  Block b
+// writes the error sum of its rows of step k to sse[k * blocks + b] and the
+// column sums of its deltas to colsum row k * blocks + b, blocks =
+// elman_window_blocks(S).  Only for elman_window_fits(...); otherwise, or
+// for a missing pointer, hipErrorInvalidValue.
+struct ElmanWindow {
+  const float* X;          // [steps * S][n_ext]
+  int n_ext;
+  const float* cont;       // [steps * S]
+  const float* mask;       // [steps * S] or nullptr (no mask)
+  const float* T;          // [steps * S][ldt]
+  int ldt;
+  const float* Hprev;      // context source of step 0: [S][ldhp], or nullptr
+  int ldhp;
+  const float* W0;         // [n0][ldw0], bias row b0
+  int ldw0;
+  const float* b0;
+  const float* W1;         // [n1][ldw1], bias row b1
+  int ldw1;
+  const float* b1;
+  int n0, n1, n2;
+  float* H;                // hidden units [steps * S][ldh]
+  int ldh;
+  float* rows;             // input rows [steps * S][ldr]
+  int ldr;
+  float* D;                // output deltas [steps * S][ldd]
+  int ldd;
+  float* colsum;           // [steps * blocks][ldcs]
+  int ldcs;
+  double* sse;             // [steps * blocks]
+  const float* tab;
+  int S, steps;
+};
+bool elman_window_fits(int S, int n_ext, int n0, int n1, int n2);
+int elman_window_blocks(int S);
+hipError_t elman_window(hipStream_t s, const ElmanWindow& w);
+
 // out[0] = sum of part[0 .. n-1] in a fixed order (double).
 hipError_t sse_reduce(hipStream_t s, const double* part, int n, double* out);
 

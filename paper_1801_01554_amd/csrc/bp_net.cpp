@@ -687,6 +687,47 @@ int ensure_seq_in(bp_net* net, int64_t rows) {
   return BP_OK;
 }
 
+// The forward pass of the window of `steps` steps starting at step w0 (of B
+// steps per window) in one launch (one hidden layer, context in order).
+int run_window(bp_net* net, const float* X, const float* targets, const float* cont, const float* mask, int64_t w0,
+               int steps, int B, int S, int per_step) {
+  const int n_ext = net->n[0] - net->n_ctx, nL = net->n[2], lda1 = net->lda[1];
+  bpk::ElmanWindow ew;
+  ew.X = n_ext > 0 ? X + (size_t)w0 * S * n_ext : nullptr;
+  ew.n_ext = n_ext;
+  ew.cont = cont + (size_t)w0 * S;
+  ew.mask = mask + (size_t)w0 * S;
+  ew.T = targets + (size_t)w0 * S * nL;
+  ew.ldt = nL;
+  // context source of the window's first step: the last step of the
+  // previous (full) window; none in the first window of the call
+  ew.Hprev = w0 > 0 ? net->act[1] + (size_t)(B - 1) * S * lda1 : nullptr;
+  ew.ldhp = lda1;
+  ew.W0 = wl(net, 0);
+  ew.ldw0 = net->ldw[0];
+  ew.b0 = wbias(net, 0);
+  ew.W1 = wl(net, 1);
+  ew.ldw1 = net->ldw[1];
+  ew.b1 = wbias(net, 1);
+  ew.n0 = net->n[0];
+  ew.n1 = net->n[1];
+  ew.n2 = nL;
+  ew.H = net->act[1];
+  ew.ldh = lda1;
+  ew.rows = net->seq_in;
+  ew.ldr = net->lda[0];
+  ew.D = net->del[2];
+  ew.ldd = net->lda[2];
+  ew.colsum = net->csum[2];
+  ew.ldcs = net->lda[2];
+  ew.sse = net->sse_part + (size_t)w0 * per_step;
+  ew.tab = net->sig_tab;
+  ew.S = S;
+  ew.steps = steps;
+  BP_LAUNCH(net, BP_K_SEQ_WIN, bpk::elman_window(net->stream, ew));
+  return BP_OK;
+}
+
 // Training over n_steps x S patterns: windows of B steps; within a window,
 // step by step: assemble the input rows (external inputs, flag x context),
 // forward pass with masked output deltas; then one backward pass and pooled
@@ -701,21 +742,26 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
   const int steps_max = (int)std::min<int64_t>(B, T);
   const int last_steps = (int)(T - (T - 1) / B * B);
   const int64_t rows_max = (int64_t)steps_max * S;
-  const int csS = bpk::colsum_rows(S);
+  const bool fuse_ctx = fuse_ctx_input(net, S);
+  // one hidden layer: the window's forward pass in one launch, each block
+  // carrying the recurrence of its own streams
+  const bool window = net->ctx_in_order && L == 2 && bpk::elman_window_fits(S, n_ext, net->n[0], net->n[1], nL);
+  // otherwise, with one hidden layer, step k's hidden layer and step k - 1's
+  // output layer share a launch; a window's first hidden layer and last
+  // output layer run alone
+  const bool pair =
+      !window && fuse_ctx && L == 2 && B > 1 && bpk::elman_pair_fits(S, net->n[0], net->n[1], net->n[2]);
+  // output-layer column-sum rows of a step, and error partials of a step
+  const int csS = window ? bpk::elman_window_blocks(S) : bpk::colsum_rows(S);
+  const int per_step = window ? bpk::elman_window_blocks(S) : bpk::output_delta_blocks(S, nL, net->n[L - 1]);
   int rc = ensure_workspace(net, rows_max, (int64_t)steps_max * csS,
                             std::max({splitk_floats(net, S, rows_max), splitk_floats(net, 0, (int64_t)last_steps * S)}));
   if (rc) return rc;
   rc = ensure_seq_in(net, rows_max);
   if (rc) return rc;
-  const int per_step = bpk::output_delta_blocks(S, nL, net->n[L - 1]);
   rc = ensure_sse(net, (size_t)T * per_step);
   if (rc) return rc;
   hipStream_t s = net->stream;
-  const bool fuse_ctx = fuse_ctx_input(net, S);
-  // one hidden layer: step k's hidden layer and step k - 1's output layer
-  // share a launch; a window's first hidden layer and last output layer run
-  // alone
-  const bool pair = fuse_ctx && L == 2 && B > 1 && bpk::elman_pair_fits(S, net->n[0], net->n[1], net->n[2]);
   const int lda1 = net->lda[1], ldL = net->lda[L];
   std::vector<float*> acts(L + 1, nullptr);
   // the output layer's view of step k of the window (step g of the call)
@@ -728,7 +774,11 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
   };
   for (int64_t w0 = 0; w0 < T; w0 += B) {
     const int steps = (int)std::min<int64_t>(B, T - w0);
-    for (int k = 0; k < steps; ++k) {
+    if (window) {
+      rc = run_window(net, X, targets, cont, mask, w0, steps, B, S, per_step);
+      if (rc) return rc;
+    }
+    for (int k = 0; k < steps && !window; ++k) {
       const int64_t g = w0 + k;
       if (pair && k > 0) {
         const OutputView ov = view(k - 1, g - 1);

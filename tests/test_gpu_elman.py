@@ -177,12 +177,15 @@ def test_sequence_arguments_are_checked(dev):
     assert L.bp_train_sequences(net._h, None, None, None, None, 0, 0, 1, 0.1, 0.9, None) == bp.BP_EINVAL
 
 
-# Context copying hidden layer 1 in order: the first product builds the step's
-# input rows itself.  Cases: external inputs not a multiple of 4 wide (scalar
-# loads), one step per window (the source rows are the ones the step writes:
-# those steps build the rows first), no external input, a context of the
-# first 24 of 40 hidden units, and a net too large for that path (2000
-# streams x 300 hidden units: assembled rows and tiled products).
+# Context copying hidden layer 1 in order: with one hidden layer of at most
+# 256 units, a window's forward pass is one launch; otherwise the first
+# product builds the step's input rows itself.  Cases: external inputs not a
+# multiple of 4 wide, one step per window (the context source rows are the
+# ones the window writes), no external input, a context of the first 24 of 40
+# hidden units (one and two hidden layers), a net too large for both (2000
+# streams x 300 hidden units: assembled rows and tiled products), one just
+# past the window's limits (step pairs), and the window's column widths and
+# largest sizes.
 BUILT_INPUT_SPECS = [
     wl.SeqSpec("elman-built-13+40", 13, (40,), 9, 40, 70, 23, 4, 3, 9, 0.01, 0.9, 2, 31),
     wl.SeqSpec("elman-built-1-step", 16, (40,), 9, 40, 70, 11, 1, 3, 9, 0.01, 0.9, 2, 32),
@@ -190,6 +193,14 @@ BUILT_INPUT_SPECS = [
     wl.SeqSpec("elman-built-8+24of40", 8, (40, 16), 9, 24, 70, 17, 5, 3, 9, 0.01, 0.9, 2, 34),
     # too many output tiles for the skinny kernel: input assembly, then the tiled products
     wl.SeqSpec("elman-tiled-10+300", 10, (300,), 7, 300, 2000, 6, 3, 2, 5, 0.001, 0.9, 1, 35),
+    # one hidden layer past the one-launch window's 256 units: step pairs in one launch
+    wl.SeqSpec("elman-pair-12+264", 12, (264,), 9, 264, 100, 11, 4, 3, 9, 0.001, 0.9, 2, 36),
+    # one-launch windows: a context of the first 24 of 40 hidden units; 8- and 16-byte weight
+    # columns per lane (100 hidden, 130 outputs); the largest sizes (256 external inputs, 256
+    # hidden units, 256 outputs)
+    wl.SeqSpec("elman-win-8+24of40", 8, (40,), 9, 24, 70, 17, 5, 3, 9, 0.01, 0.9, 2, 37),
+    wl.SeqSpec("elman-win-30+100-130", 30, (100,), 130, 100, 45, 7, 3, 2, 5, 0.01, 0.9, 2, 38),
+    wl.SeqSpec("elman-win-256+256-256", 256, (256,), 256, 256, 37, 6, 3, 2, 5, 0.001, 0.9, 1, 39),
 ]
 
 
@@ -211,3 +222,16 @@ def test_input_built_in_product_matches_oracle(dev, spec):
     err = float(np.max(np.abs(y - ref)))
     _say(f"  forward max abs err {err}")
     assert err <= FWD_TOL
+
+
+def test_elman_runs_are_identical(dev):
+    w = wl.make_sequences("elman-20+48-48-12")
+    s = w.spec
+    out = []
+    for _ in range(2):
+        net, _o = _pair(w)
+        x, t, c, m = _dev_arrays(w, dev)
+        sse = net.train_sequences(x, t, c, m, s.steps_per_update, w.lr, w.momentum)
+        out.append((sse, net.get_weights()))
+    assert out[0][0] == out[1][0]
+    np.testing.assert_array_equal(out[0][1], out[1][1])
