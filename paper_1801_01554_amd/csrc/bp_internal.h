@@ -204,7 +204,7 @@ hipError_t seq_assemble(hipStream_t s, const float* X, int n_ext, const float* c
 // blocks.  Step k of the window is rows k * S .. k * S + S - 1 of H, rows, D
 // (and of X, cont, mask, T, each given at the window's first step).  Block b
 // writes the error sum of its rows of step k to sse[k * blocks + b] and the
-// column sums of its deltas to colsum row k * blocks + b, blocks =
+// column sums of its deltas over the whole window to colsum row b, blocks =
 // elman_window_blocks(S).  Only for elman_window_fits(...); otherwise, or
 // for a missing pointer, hipErrorInvalidValue.
 struct ElmanWindow {
@@ -229,7 +229,7 @@ struct ElmanWindow {
   int ldr;
   float* D;                // output deltas [steps * S][ldd]
   int ldd;
-  float* colsum;           // [steps * blocks][ldcs]
+  float* colsum;           // [blocks][ldcs]
   int ldcs;
   double* sse;             // [steps * blocks]
   const float* tab;

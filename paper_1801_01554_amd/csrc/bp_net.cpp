@@ -751,7 +751,8 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
   // output layer run alone
   const bool pair =
       !window && fuse_ctx && L == 2 && B > 1 && bpk::elman_pair_fits(S, net->n[0], net->n[1], net->n[2]);
-  // output-layer column-sum rows of a step, and error partials of a step
+  // output-layer column-sum rows of a step (of a window for the one-launch
+  // window), and error partials of a step
   const int csS = window ? bpk::elman_window_blocks(S) : bpk::colsum_rows(S);
   const int per_step = window ? bpk::elman_window_blocks(S) : bpk::output_delta_blocks(S, nL, net->n[L - 1]);
   int rc = ensure_workspace(net, rows_max, (int64_t)steps_max * csS,
@@ -825,7 +826,7 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
     BatchInput win;
     win.x = net->seq_in;
     win.ldx = net->lda[0];
-    rc = run_backward_update(net, win, steps * S, lr, mom, steps * csS);
+    rc = run_backward_update(net, win, steps * S, lr, mom, window ? csS : steps * csS);
     if (rc) return rc;
   }
   BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(s, net->sse_part, (int)(T * per_step), net->sse_dev));

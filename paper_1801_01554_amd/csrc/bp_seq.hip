@@ -287,14 +287,18 @@ __global__ __launch_bounds__(kWinThreads) void elman_window_kernel(ElmanWindow p
       if (lane == 0) maskC[i] = mr[i];
     }
   };
-  // wave 4: deltas, column sums and error partial of step k from LDS
+  // wave 4: deltas and error partial of step k from LDS; the column sums
+  // added over the window's steps in step order
+  float cacc[kWinMaxUnits / 64] = {};
   auto io_store_d = [&](int k) {
     const size_t row0 = (size_t)k * S + m0;
     for (int i = 0; i < rows_in; ++i)
       for (int c = 4 * lane; c < n2; c += 256)
         *reinterpret_cast<f32x4*>(p.D + (row0 + i) * p.ldd + c) = *reinterpret_cast<const f32x4*>(Dl + i * US + c);
     const size_t crow = (size_t)k * gridDim.x + blockIdx.x;
-    for (int c = lane; c < n2; c += 64) p.colsum[crow * p.ldcs + c] = csl[c];
+#pragma unroll
+    for (int q = 0; q < kWinMaxUnits / 64; ++q)
+      if (lane + 64 * q < n2) cacc[q] += csl[lane + 64 * q];
     // error partial: the compute threads' sums added in thread order
     double e = 0.0;
     for (int c = lane; c < n2; c += 64) e += (double)ssl[c];
@@ -436,7 +440,12 @@ __global__ __launch_bounds__(kWinThreads) void elman_window_kernel(ElmanWindow p
     }
     __syncthreads();
   }
-  if (io) io_store_d(steps - 1);
+  if (io) {
+    io_store_d(steps - 1);
+#pragma unroll
+    for (int q = 0; q < kWinMaxUnits / 64; ++q)
+      if (lane + 64 * q < n2) p.colsum[(size_t)blockIdx.x * p.ldcs + lane + 64 * q] = cacc[q];
+  }
 }
 
 template <int RG, int C1>
