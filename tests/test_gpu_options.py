@@ -90,6 +90,7 @@ def test_table_forward_matches_oracle(dev, sizes, n, onehot):
 
 
 @pytest.mark.parametrize("sizes,n,batch,onehot", [((203, 120, 26), 512, 512, True),    # fused small-net path
+                                                  ((203, 120, 26), 40, 16, True),      # fused path, batches of 16
                                                   ((203, 300, 26), 300, 300, True),    # one-hot gather/scatter
                                                   ((70, 45, 9), 300, 100, False),      # dense products
                                                   ((64, 1100, 16), 256, 256, False)])  # split-K output layer
@@ -124,6 +125,7 @@ def _poison_case(sizes, n, onehot, seed):
 # (sizes, n, batch, onehot, poison): every update kernel
 POISON_CASES = [
     ((203, 120, 26), 64, 64, True, np.nan),        # fused small-net update
+    ((203, 120, 26), 16, 16, True, np.nan),        # fused small-net update, a batch of 16
     ((203, 300, 26), 96, 96, True, 1e30),          # one-hot scatter + dense output change
     ((70, 45, 9), 200, 200, False, 1e30),          # dense change products (fused update epilogue)
     ((40, 30, 20), 2048, 2048, False, np.nan),     # split-K change (skinny kernel) + bias rows

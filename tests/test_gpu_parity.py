@@ -167,6 +167,25 @@ def test_fused_path_active_counts(dev, n_active):
     _check_update(w, dev, 512, 0.05, 0.9, what=f"fused path, {n_active} active inputs")
 
 
+# Small batches on the fused path: one update, several updates with a short
+# last batch, the largest layer sizes, single units, batches of one pattern,
+# and a call whose last batch alone is small.
+@pytest.mark.parametrize("sizes,n,batch", [((203, 120, 26), 16, 16), ((203, 120, 26), 37, 16),
+                                           ((203, 120, 26), 32, 16), ((203, 256, 64), 45, 15),
+                                           ((50, 1, 1), 9, 1), ((203, 40, 7), 108, 100)])
+def test_small_batch_updates(dev, sizes, n, batch):
+    w = wl.make_custom(sizes, n, seed=n + batch + sizes[1], onehot=True, init="uniform0.3")
+    _check_update(w, dev, batch, 0.05, 0.9, what="small-batch updates")
+
+
+@pytest.mark.parametrize("n_active", [1, 12, 32])
+def test_small_batch_active_counts(dev, n_active):
+    w = wl.make_custom((203, 120, 26), 40, seed=80 + n_active, onehot=True, init="uniform0.3")
+    g = np.random.default_rng(100 + n_active)
+    w.active = np.stack([g.permutation(203)[:n_active] for _ in range(40)]).astype(np.int32)
+    _check_update(w, dev, 16, 0.05, 0.9, what=f"batches of 16, {n_active} active inputs")
+
+
 # --------------------------------------------------------------------------- epochs
 @pytest.mark.parametrize("name", ["nettalk-80-b1024", "nettalk-120-b512", "nettalk-120-b16"])
 def test_epoch_errors_nettalk(dev, name):
@@ -230,6 +249,7 @@ def test_onehot_path_equals_dense_path(dev):
 # Out-of-range one-hot indices select no weight row: training and the
 # forward pass equal the oracle's dense path on the 0/1 inputs without them.
 @pytest.mark.parametrize("sizes,n,batch", [((203, 120, 26), 300, 100),    # fused small-net path
+                                           ((203, 120, 26), 50, 10),      # fused path, batches of 10
                                            ((203, 300, 26), 200, 200)])   # gather + scatter kernels
 def test_onehot_out_of_range_indices_select_nothing(dev, sizes, n, batch):
     w = wl.make_custom(sizes, n, seed=5 + n, onehot=True, init="uniform0.3")
@@ -258,7 +278,7 @@ def test_onehot_out_of_range_indices_select_nothing(dev, sizes, n, batch):
     net.close()
 
 
-@pytest.mark.parametrize("name,n", [("nettalk-120-b512", 2048), ("deep-512-2048x3-64", 8192)])
+@pytest.mark.parametrize("name,n", [("nettalk-120-b512", 2048), ("nettalk-120-b16", 400), ("deep-512-2048x3-64", 8192)])
 def test_run_to_run_identical(dev, name, n):
     w = wl.make(name, n_patterns=n)
     _say(f"case determinism {name} n={n}")
