@@ -198,6 +198,9 @@ def elman_window(sizes, n_ctx, S):
 def change_splits(M, N, K):
     """Mirror of the library's split count for a change product (split over blocks, whose last
     block per tile applies the update), for work accounting only."""
+    t64 = -(-M // 64) * -(-N // 64)
+    if K >= 4096 and 16 <= t64 < 128:
+        return min(-(-256 // t64), K // 256)
     if K >= 1024 and -(-M // 64) * -(-N // 64) < 128:
         tiles, chunk = -(-M // 64) * -(-N // 32), 1024
         while chunk > 128 and tiles * -(-K // chunk) < 256:

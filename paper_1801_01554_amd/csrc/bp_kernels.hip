@@ -1487,9 +1487,17 @@ struct ChangePlan {
   int chunk;
   int tiles;        // output tiles
   int tile_elems;   // floats per output tile
+  bool tiles64 = false;  // 64 x 64 tiles on gemm_kernel
 };
 
 ChangePlan change_plan(int M, int N, int K) {
+  // long K over 16-127 output tiles of 64 x 64: those tiles split over K on
+  // about one block per CU
+  if (K >= 4096 && tiles_of(M, N, 64) >= 16 && tiles_of(M, N, 64) < 128) {
+    const int tiles = tiles_of(M, N, 64);
+    const int sp = std::min((kCUs + tiles - 1) / tiles, K / 256);
+    return {false, sp, chunk_for(K, sp), tiles, 64 * 64, true};
+  }
   if (K >= 1024 && tiles_of(M, N, 64) < 128) {
     const int tiles = ((M + 63) / 64) * ((N + 31) / 32);
     int chunk = 1024;
@@ -1524,6 +1532,7 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
   }
   if (!arrivals || !ws || pl.tiles > kMaxArrivals) return hipErrorInvalidValue;
   EpiSplitUpdate e{ws, W, V, ldw, lr, mom, limit, faults, arrivals, pl.splits};
+  if (pl.tiles64) return launch_gemm<64, 64, kTileK, true, false>(s, A, lda, D, ldd, M, N, K, pl.splits, pl.chunk, e);
   if (pl.skinny)
     return launch_kernel(skinny_kernel<2, true, false, false, false, false, EpiSplitUpdate>, pl.tiles * pl.splits, 512,
                          0, s, A, lda, D, ldd, M, N, K, pl.chunk, e, CtxInput{});

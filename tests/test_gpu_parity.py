@@ -133,6 +133,8 @@ def test_first_update_full_size(dev, name):
     # splits and applying the update: 2 splits (the second ragged) and 8 splits
     ((2000, 2100, 10), 1100, 1100, False),
     ((800, 800, 3), 2100, 2100, False),
+    # change product over 25 tiles of 64 x 64 split over K = 4500 (the last split ragged)
+    ((300, 260, 20), 4500, 4500, False),
     # sigmoid and hidden-delta products of 256 one-block 256 x 256 tiles (4096 x 4096 outputs, K a
     # multiple of 32), and the same outputs with K = 40 and 100, which stay on 128 x 128 tiles
     ((96, 4096, 32), 4096, 4096, False),
