@@ -485,6 +485,47 @@ def summarize_stats(src, out, title, note, cmd):
         f.write("\n".join(lines) + "\n")
 
 
+def summarize_mfma(counter_csv, trace_csv, out, title, note, cmd):
+    """Writes the MFMA-pipe utilisation per kernel from a rocprofv3 --pmc GRBM_GUI_ACTIVE
+    SQ_VALU_MFMA_BUSY_CYCLES (+ --kernel-trace) run as the markdown summary kept in profiles/:
+    the clock a dispatch ran at (GRBM_GUI_ACTIVE summed over the 8 XCDs / 8 / duration) and
+    the share of those cycles the MFMA pipes were busy (SQ_VALU_MFMA_BUSY_CYCLES summed over
+    the 1024 SIMDs / 1024 / (GRBM_GUI_ACTIVE / 8))."""
+    import collections
+    import csv
+    import math
+    import re
+    dur = {r["Dispatch_Id"]: int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in csv.DictReader(open(trace_csv))}
+    per = collections.defaultdict(dict)
+    for r in csv.DictReader(open(counter_csv)):
+        per[r["Dispatch_Id"]][r["Counter_Name"]] = float(r["Counter_Value"])
+        per[r["Dispatch_Id"]]["name"] = r["Kernel_Name"]
+        per[r["Dispatch_Id"]]["grid"] = f'{r.get("Grid_Size", r.get("Grid_Size_X", ""))}'
+    agg = collections.defaultdict(list)
+    for d, v in per.items():
+        if d not in dur or "GRBM_GUI_ACTIVE" not in v or "SQ_VALU_MFMA_BUSY_CYCLES" not in v:
+            continue
+        name = v["name"].replace("bpk::(anonymous namespace)::", "")
+        m = re.search(r"(\w+_kernel(?:<[^>]*>)?)", name)
+        if not m or "gemm" not in m.group(1) and "skinny" not in m.group(1) and "elman" not in m.group(1):
+            continue
+        # launches of one kernel differ by shape: grouped by duration to within 10%
+        key = (m.group(1), round(math.log(dur[d]) / math.log(1.1)))
+        g = v["GRBM_GUI_ACTIVE"] / 8.0
+        agg[key].append((dur[d], g / dur[d], v["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024.0 / g))
+    lines = [f"# {title}", "", note, "", "Command (on the MI355X box, from /tmp with TMPDIR=/tmp; R = repository root):",
+             "", f"    {cmd}", "", "| kernel | dispatches | average µs | clock GHz | MFMA busy |", "|---|---|---|---|---|"]
+    for (k, _), v in sorted(agg.items(), key=lambda kv: -sum(x[0] for x in kv[1])):
+        n = len(v)
+        avg = sum(x[0] for x in v) / n
+        if n < 4 or avg < 20e3:    # short launches: the counters' window is longer than the dispatch
+            continue
+        lines.append(f"| `{k}` | {n} | {avg / 1e3:.1f} | {sum(x[1] for x in v) / n:.2f} | "
+                     f"{100 * sum(x[2] for x in v) / n:.1f}% |")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def copy_calibration():
     """Copies a 1 GiB buffer four times (device to device), for the FETCH_SIZE / WRITE_SIZE scale."""
     import torch
@@ -591,11 +632,16 @@ def main():
     ap.add_argument("--counters-to-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH", "CAL_WRITE"),
                     help="write per-launch HBM traffic of --workload to profiles/traffic.json")
     ap.add_argument("--command", default="", help="the profiling command recorded with --counters-to-traffic")
+    ap.add_argument("--summarize-mfma", nargs=6, metavar=("COUNTER_CSV", "TRACE_CSV", "OUT_MD", "TITLE", "NOTE", "CMD"),
+                    help="write the MFMA-busy summary of a rocprofv3 --pmc run")
     ap.add_argument("--summarize-stats", nargs=5, metavar=("STATS_CSV", "OUT_MD", "TITLE", "NOTE", "CMD"),
                     help="format a rocprofv3 kernel_stats.csv as a profiles/ summary")
     args = ap.parse_args()
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
         return
     if args.counters_to_traffic:
         counters_to_traffic(args.workload, *args.counters_to_traffic, args.command)
