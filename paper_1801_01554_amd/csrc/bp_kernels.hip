@@ -327,6 +327,45 @@ __device__ __forceinline__ void store_tile(float* lds, const f32x4* r, int tid) 
   }
 }
 
+// A TO x TD tile (TD contiguous, inside the matrix) copied from global memory
+// straight into its LDS image [TO][S] by the LDS-DMA load: one wave
+// instruction writes 64 consecutive 16-byte chunks of the image (lane l the
+// l-th), each lane loading its chunk's global address.  The image is taken in
+// blocks of 64 chunks, block b by wave b % NW; a chunk of row padding
+// (S - TD floats per row) loads a copy of the row's last data chunk.  Its
+// global offsets relative to the tile origin are fixed across K stages, so
+// they are computed once (off) and a stage passes the origin.
+template <int TO, int TD, int S, int NTH>
+struct DmaTile {
+  static constexpr int CPR = S / 4;                   // chunks per image row
+  static constexpr int Q = TO * CPR;                  // chunks
+  static constexpr int NB = (Q + 63) / 64;            // 64-chunk blocks
+  static constexpr int NW = NTH / 64;
+  static constexpr int PER = (NB + NW - 1) / NW;      // blocks per wave (at most)
+  static_assert(S % 4 == 0 && TD % 4 == 0 && S >= TD, "DMA tile shape");
+  int off[PER];                                       // element offsets from the origin
+  __device__ __forceinline__ void init(int ld, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = min((wave + i * NW) * 64 + lane, Q - 1);
+      const int row = q / CPR, c = min(q % CPR, TD / 4 - 1);
+      off[i] = row * ld + 4 * c;
+    }
+  }
+  // the tile with origin `org` (global) into the image `lds`
+  __device__ __forceinline__ void copy(const float* org, float* lds, int wave, int lane) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int b = wave + i * NW;
+#if defined(__HIP_DEVICE_COMPILE__)   // (a device instruction: the host pass only sees the kernel's signature)
+      if (b < NB && (b < NB - 1 || lane < Q - 64 * (NB - 1)))
+        __builtin_amdgcn_global_load_lds(org + off[i],
+                                         (__attribute__((address_space(3))) void*)(lds + 256 * b), 16, 0, 0);
+#endif
+    }
+  }
+};
+
 // Maps the hardware block index to a tile.  Blocks reach the eight XCDs
 // round-robin (hardware index mod 8); each XCD is given a contiguous range
 // of the tile order, and the tile order walks groups of 8 tile rows column by
@@ -458,7 +497,7 @@ __global__ __launch_bounds__(NTH) void gemm_kernel(const float* __restrict__ A, 
     if (s + 1 < nst) store_stage((s + 1) & 1, rsa, rsb);
     __syncthreads();
   };
-  if constexpr (NTH != kThreads) {
+  if constexpr (NTH != kThreads && B_NK) {
     // 512-thread blocks hold twice the accumulators per wave; one register
     // set suffices there, as a stage is twice the MFMA work per SIMD (two
     // waves of 128 x 64 each): the load of stage s + 1 lands while stage s
@@ -472,6 +511,34 @@ __global__ __launch_bounds__(NTH) void gemm_kernel(const float* __restrict__ A, 
       if (s + 1 < nst) load_stage(kb + (s + 1) * BK, ra0, rb0);
       compute(s & 1);
       if (s + 1 < nst) store_stage((s + 1) & 1, ra0, rb0);
+      __syncthreads();
+    }
+  } else if constexpr (NTH != kThreads) {
+    // The sigmoid products' 512-thread blocks (whole tiles only) copy each
+    // stage straight into LDS with the LDS-DMA load: stage s + 1 is copied
+    // into the other buffer while stage s is multiplied, and the barrier that
+    // ends stage s waits for the copy; no staging registers, no LDS stores.
+    // (Measured: forward products 1.3% faster; the hidden-delta products, whose
+    // B tile is also sliced into 128-byte rows, 3% slower, so they stage
+    // through registers.)
+    DmaTile<A_KM ? BK : BM, A_KM ? BM : BK, T::SA, NTH> da;
+    DmaTile<B_NK ? BN : BK, B_NK ? BK : BN, T::SB, NTH> db;
+    da.init(lda, wave, lane);
+    db.init(ldb, wave, lane);
+    // stage origins: the tile's first row and column at depth k
+    auto a_org = [&](int k) { return A_KM ? A + (size_t)k * lda + m0 : A + (size_t)m0 * lda + k; };
+    auto b_org = [&](int k) { return B_NK ? B + (size_t)n0 * ldb + k : B + (size_t)k * ldb + n0; };
+    if (nst > 0) {
+      da.copy(a_org(kb), As[0], wave, lane);
+      db.copy(b_org(kb), Bs[0], wave, lane);
+      __syncthreads();
+    }
+    for (int s = 0; s < nst; ++s) {
+      if (s + 1 < nst) {
+        da.copy(a_org(kb + (s + 1) * BK), As[(s + 1) & 1], wave, lane);
+        db.copy(b_org(kb + (s + 1) * BK), Bs[(s + 1) & 1], wave, lane);
+      }
+      compute(s & 1);
       __syncthreads();
     }
   } else {
