@@ -126,10 +126,25 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
                          int K, float* W, float* V, int ldw, float lr, float mom, float* ws, int* arrivals,
                          float limit, unsigned long long* faults);
 
-// Bias-row change and update: G[n] = sum_{k < rows} D[k][n];  V = lr G + mom V;  W += V.
-// D is the per-tile column-sum buffer of the deltas (rows = colsum_rows(batch)).
-hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb,
-                       float lr, float mom, float limit, unsigned long long* faults);
+// Bias-row change and update of one layer: G[n] = sum_{k < rows} D[k][n];
+// V = lr G + mom V;  W += V.  D is the per-tile column-sum buffer of the
+// deltas (rows = colsum_rows(batch)); Wb, Vb the bias rows of W and V.
+struct BiasJob {
+  const float* D;
+  float* Wb;
+  float* Vb;
+  int ldd, rows, N;
+  int block0;   // set by bias_update
+};
+constexpr int kMaxBiasJobs = 8;
+struct BiasJobs {
+  BiasJob j[kMaxBiasJobs];
+  int n;
+};
+// The bias updates of n layers (independent: distinct D, Wb, Vb), up to
+// kMaxBiasJobs per launch.
+hipError_t bias_update(hipStream_t s, const BiasJob* jobs, int n, float lr, float mom, float limit,
+                       unsigned long long* faults);
 
 // One-hot first layer: net[p][j] = W0[n0][j] + sum_{k < n_active} W0[act[p][k]][j].
 // mode 0: out[p][j] = sigma(net).  mode 1 (single-layer nets, training):

@@ -1247,18 +1247,23 @@ __global__ __launch_bounds__(kFin) void output_finish_kernel(const float* __rest
   }
 }
 
-// Bias-row change: column sums of D over `rows` rows, then the update.  Block
-// = 1024 threads = 16 waves; lane = column within a 64-column strip; wave w
-// sums its contiguous share of the rows in order, then the 16 partial sums
-// are added in wave order.
+// Bias-row changes of several layers in one launch: column sums of each
+// layer's D over its `rows` rows, then the update.  Blocks [block0, next
+// job's block0) take the job's 64-column strips.  Block = 1024 threads = 16
+// waves; lane = column within a strip; wave w sums its contiguous share of
+// the rows in order, then the 16 partial sums are added in wave order.
 constexpr int kBiasWaves = 16;
-__global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(const float* __restrict__ D, int ldd,
-                                                                       int rows, int N, float* Wb, float* Vb,
-                                                                       float lr, float mom, float limit,
-                                                                       unsigned long long* faults) {
+__global__ __launch_bounds__(64 * kBiasWaves) void bias_update_kernel(BiasJobs jobs, float lr, float mom,
+                                                                       float limit, unsigned long long* faults) {
   __shared__ float part[kBiasWaves][64];
+  int q = 0;
+  while (q + 1 < jobs.n && (int)blockIdx.x >= jobs.j[q + 1].block0) ++q;
+  const float* __restrict__ D = jobs.j[q].D;
+  float* Wb = jobs.j[q].Wb;
+  float* Vb = jobs.j[q].Vb;
+  const int ldd = jobs.j[q].ldd, rows = jobs.j[q].rows, N = jobs.j[q].N;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 64 + lane;
+  const int n = ((int)blockIdx.x - jobs.j[q].block0) * 64 + lane;
   const int r0 = (int)((int64_t)rows * wave / kBiasWaves), r1 = (int)((int64_t)rows * (wave + 1) / kBiasWaves);
   float s = 0.f;
   if (n < N) {
@@ -1606,11 +1611,23 @@ hipError_t change_update(hipStream_t s, const float* A, int lda, const float* D,
   return launch_cfg<true, false>(s, A, lda, D, ldd, M, N, K, pl.splits, pl.chunk, e);
 }
 
-hipError_t bias_update(hipStream_t s, const float* D, int ldd, int rows, int N, float* Wb, float* Vb, float lr,
-                       float mom, float limit, unsigned long long* faults) {
-  if (N <= 0) return hipSuccess;
-  return launch_kernel(bias_update_kernel, (N + 63) / 64, 64 * kBiasWaves, 0, s, D, ldd, rows, N, Wb, Vb, lr, mom,
-                       limit, faults);
+hipError_t bias_update(hipStream_t s, const BiasJob* jobs, int n, float lr, float mom, float limit,
+                       unsigned long long* faults) {
+  for (int j0 = 0; j0 < n; j0 += kMaxBiasJobs) {
+    BiasJobs b{};
+    int blocks = 0;
+    for (int j = j0; j < n && j < j0 + kMaxBiasJobs; ++j) {
+      if (jobs[j].N <= 0) continue;
+      b.j[b.n] = jobs[j];
+      b.j[b.n].block0 = blocks;
+      blocks += (jobs[j].N + 63) / 64;
+      ++b.n;
+    }
+    if (blocks == 0) continue;
+    const hipError_t e = launch_kernel(bias_update_kernel, blocks, 64 * kBiasWaves, 0, s, b, lr, mom, limit, faults);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int onehot_forward_blocks(int rows, int H) {

@@ -401,9 +401,12 @@ int run_small(bp_net* net, const BatchInput& in, int rows, const float* T, doubl
 }
 
 // Backward pass and update of one batch whose deltas of the output layer are
-// in del[L].
+// in del[L].  The bias rows, which no delta or change product reads, are
+// updated together in one launch after the last change product.
 int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, float mom, int top_csum = 0) {
   hipStream_t s = net->stream;
+  bpk::BiasJob bias[bpk::kMaxBiasJobs];
+  int nb = 0;
   for (int l = net->L - 1; l >= 0; --l) {
     // Hidden deltas of layer l use W_l before its update.
     if (l >= 1)
@@ -424,11 +427,14 @@ int run_backward_update(bp_net* net, const BatchInput& in, int rows, float lr, f
               bpk::change_update(s, A, ldA, net->del[l + 1], net->lda[l + 1], net->n[l], net->n[l + 1], rows,
                                  wl(net, l), vl(net, l), net->ldw[l], lr, mom, net->splitk, net->arrivals,
                                  net->fault_limit, net->faults));
-    BP_LAUNCH(net, BP_K_BIAS,
-              bpk::bias_update(s, net->csum[l + 1], net->lda[l + 1],
-                               (l + 1 == net->L && top_csum > 0) ? top_csum : bpk::colsum_rows(rows), net->n[l + 1],
-                               wbias(net, l), vbias(net, l), lr, mom, net->fault_limit, net->faults));
+    bias[nb++] = {net->csum[l + 1], wbias(net, l), vbias(net, l), net->lda[l + 1],
+                  (l + 1 == net->L && top_csum > 0) ? top_csum : bpk::colsum_rows(rows), net->n[l + 1], 0};
+    if (nb == bpk::kMaxBiasJobs) {
+      BP_LAUNCH(net, BP_K_BIAS, bpk::bias_update(s, bias, nb, lr, mom, net->fault_limit, net->faults));
+      nb = 0;
+    }
   }
+  if (nb > 0) BP_LAUNCH(net, BP_K_BIAS, bpk::bias_update(s, bias, nb, lr, mom, net->fault_limit, net->faults));
   return BP_OK;
 }
 

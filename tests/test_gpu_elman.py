@@ -201,6 +201,11 @@ BUILT_INPUT_SPECS = [
     wl.SeqSpec("elman-win-8+24of40", 8, (40,), 9, 24, 70, 17, 5, 3, 9, 0.01, 0.9, 2, 37),
     wl.SeqSpec("elman-win-30+100-130", 30, (100,), 130, 100, 45, 7, 3, 2, 5, 0.01, 0.9, 2, 38),
     wl.SeqSpec("elman-win-256+256-256", 256, (256,), 256, 256, 37, 6, 3, 2, 5, 0.001, 0.9, 1, 39),
+    # 16-byte weight columns with W1 in LDS (129-256 hidden units, at most 64 outputs, as in
+    # the 1024-stream workload): a ragged stream count, external inputs not a multiple of 4
+    # wide, a short last window; and a context of the first 150 of 180 hidden units
+    wl.SeqSpec("elman-win-21+200-50", 21, (200,), 50, 200, 45, 7, 3, 2, 5, 0.01, 0.9, 2, 40),
+    wl.SeqSpec("elman-win-16+150of180-33", 16, (180,), 33, 150, 30, 8, 4, 2, 6, 0.01, 0.9, 2, 41),
 ]
 
 

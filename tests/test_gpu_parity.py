@@ -139,6 +139,8 @@ def test_first_update_full_size(dev, name):
     # multiple of 32), and the same outputs with K = 40 and 100, which stay on 128 x 128 tiles
     ((96, 4096, 32), 4096, 4096, False),
     ((100, 4096, 40), 4096, 4096, False),
+    # eleven weight layers: the bias rows are updated eight layers per launch, so two launches
+    ((30, 17, 40, 9, 33, 20, 12, 50, 7, 25, 16, 5), 300, 130, False),
 ])
 def test_update_ragged_shapes(dev, sizes, n, batch, onehot):
     w = wl.make_custom(sizes, n, seed=n + batch, onehot=onehot, input_kind="uniform",
