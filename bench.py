@@ -451,17 +451,12 @@ def traffic_for(workload, kind):
 def kind_of_kernel(name):
     """Kernel kind of a rocprofv3 kernel name."""
     import re
-    m = re.search(r"gemm_kernel<\d+, \d+, \d+, (true|false), (true|false), (true|false), (true|false), [^>]*?(\w+)>", name)
+    # the epilogue is the template argument named Epi...; the tile shape and a
+    # thread count may stand before or after it
+    m = re.search(r"(gemm_kernel|skinny_kernel)<[^>]*?\b(Epi\w+)", name)
     if m:
-        epi = m.group(5)
-        if epi == "EpiPartial":
-            return "output"
-        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
-                "EpiUpdate": "change", "EpiSplitUpdate": "splitk"}.get(epi)
-    m = re.search(r"skinny_kernel<\d+, [^>]*?(\w+)>", name)
-    if m:
-        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiHiddenDelta": "backward",
-                "EpiSplitUpdate": "splitk"}.get(m.group(1))
+        return {"EpiSigmoid": "forward", "EpiOutputDelta": "output", "EpiPartial": "output",
+                "EpiHiddenDelta": "backward", "EpiUpdate": "change", "EpiSplitUpdate": "splitk"}.get(m.group(2))
     for k, v in KERNEL_NAMES.items():
         if "<" not in v and v in name:
             return k
