@@ -91,9 +91,10 @@ __host__ __device__ __forceinline__ size_t small_fwdbwd_lds_floats(int P, int H,
 // the padded extents HP = small_hp(H) and OP = small_op(O) are template
 // parameters: every LDS read of the sums below uses a constant offset from
 // one base address, and the staging loop has a fixed trip count.
-//   round 1   each gather item's active indices, then targets, the bias
-//             row and W1 (HP OP / 1024 elements per thread), then the
-//             gather's W0 rows as soon as their indices arrive;
+//   loads     one issue of global loads: each gather item's active
+//             indices, then targets, the bias row and W1 (HP OP / 1024
+//             elements per thread), then the gather's W0 rows as soon as
+//             their indices arrive;
 //   gather    one (pattern, hidden unit) pair per thread: bias + the active
 //             rows of W0, in index order -> sigma;
 //   output    each output (p, c) summed by 16 adjacent lanes, lane k over
