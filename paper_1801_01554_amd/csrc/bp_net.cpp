@@ -48,6 +48,7 @@ struct bp_net {
   double* sse_part = nullptr;
   size_t sse_cap = 0;
   double* sse_dev = nullptr;
+  double* host_sse = nullptr;         // pinned host word: the error sum's read-back
   // options (section 4.3 table sigmoid; section 8 range check)
   float* sig_tab = nullptr;           // device table, set while the table sigmoid is selected
   float* sig_tab_mem = nullptr;       // its allocation (kept once made)
@@ -168,6 +169,16 @@ int hip_fail(const bp_net* net, hipError_t e, const char* what) {
     hipError_t e_ = (expr);                                 \
     if (e_ != hipSuccess) return hip_fail((net), e_, #expr); \
   } while (0)
+
+// The call's error sum: copied from the device into the net's pinned host
+// word (a copy into pageable memory goes through a staging path and costs
+// more than the whole update of a small net), then the stream is waited for.
+int read_sse(bp_net* net, const double* src, hipStream_t s, double* sse_out) {
+  BP_HIP(net, hipMemcpyAsync(net->host_sse, src, sizeof(double), hipMemcpyDeviceToHost, s));
+  BP_HIP(net, hipStreamSynchronize(s));
+  *sse_out = *net->host_sse;
+  return BP_OK;
+}
 
 // Weight, activation and delta rows are padded to 32 floats, one 128-byte
 // cache line: a row that one block writes then shares no line with a row
@@ -558,10 +569,7 @@ int train(bp_net* net, const BatchInput& in, const float* targets, int64_t n, in
     rc = train_launches(net, in, targets, n, batch, lr, mom);
     if (rc) return rc;
   }
-  if (sse_out) {
-    BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, net->stream));
-    BP_HIP(net, hipStreamSynchronize(net->stream));
-  }
+  if (sse_out) return read_sse(net, net->sse_dev, net->stream, sse_out);
   return BP_OK;
 }
 
@@ -642,10 +650,7 @@ int train_noalloc(bp_net* net, const BatchInput& in, const float* targets, int64
   net->sse_dev = sse_dev;
   net->prof = prof;
   if (rc) return rc;
-  if (sse_out) {
-    BP_HIP(net, hipMemcpyAsync(sse_out, sum, sizeof(double), hipMemcpyDeviceToHost, net->stream));
-    BP_HIP(net, hipStreamSynchronize(net->stream));
-  }
+  if (sse_out) return read_sse(net, sum, net->stream, sse_out);
   return BP_OK;
 }
 
@@ -836,10 +841,7 @@ int train_sequences(bp_net* net, const float* X, const float* targets, const flo
     if (rc) return rc;
   }
   BP_LAUNCH(net, BP_K_REDUCE, bpk::sse_reduce(s, net->sse_part, (int)(T * per_step), net->sse_dev));
-  if (sse_out) {
-    BP_HIP(net, hipMemcpyAsync(sse_out, net->sse_dev, sizeof(double), hipMemcpyDeviceToHost, s));
-    BP_HIP(net, hipStreamSynchronize(s));
-  }
+  if (sse_out) return read_sse(net, net->sse_dev, s, sse_out);
   return BP_OK;
 }
 
@@ -969,6 +971,7 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
   if (e == hipSuccess) e = hipMemset(net->V, 0, sizeof(float) * net->wtotal);
   if (e == hipSuccess) e = hipMalloc(&net->arrivals, sizeof(int) * bpk::kMaxArrivals);
   if (e == hipSuccess) e = hipMemset(net->arrivals, 0, sizeof(int) * bpk::kMaxArrivals);
+  if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&net->host_sse), sizeof(double), hipHostMallocDefault);
   if (e == hipSuccess) (void)scratch_on(net->device, &e);   // this device's scratch address, once
   if (e != hipSuccess) {
     hip_fail(nullptr, e, "bp_create");
@@ -976,6 +979,7 @@ int bp_create(const int32_t* layer_sizes, int32_t n_layers, bp_net** out) {
     free_ptr(net->W);
     free_ptr(net->V);
     free_ptr(net->arrivals);
+    if (net->host_sse) (void)hipHostFree(net->host_sse);
     delete net;
     return code;
   }
@@ -1001,6 +1005,7 @@ void bp_destroy(bp_net* net) {
   free_ptr(net->W);
   free_ptr(net->V);
   free_ptr(net->arrivals);
+  if (net->host_sse) (void)hipHostFree(net->host_sse);
   for (auto& r : net->recs) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
