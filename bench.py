@@ -483,9 +483,9 @@ def summarize_stats(src, out, title, note, cmd):
 def summarize_mfma(counter_csv, trace_csv, out, title, note, cmd):
     """Writes the MFMA-pipe utilisation per kernel from a rocprofv3 --pmc GRBM_GUI_ACTIVE
     SQ_VALU_MFMA_BUSY_CYCLES (+ --kernel-trace) run as the markdown summary kept in profiles/:
-    the clock a dispatch ran at (GRBM_GUI_ACTIVE summed over the 8 XCDs / 8 / duration) and
-    the share of those cycles the MFMA pipes were busy (SQ_VALU_MFMA_BUSY_CYCLES summed over
-    the 1024 SIMDs / 1024 / (GRBM_GUI_ACTIVE / 8))."""
+    the rate of GRBM_GUI_ACTIVE cycles during a dispatch (summed over the 8 XCDs / 8 /
+    duration) and the share of those cycles the MFMA pipes were busy
+    (SQ_VALU_MFMA_BUSY_CYCLES summed over the 1024 SIMDs / 1024 / (GRBM_GUI_ACTIVE / 8))."""
     import collections
     import csv
     import math
@@ -509,7 +509,7 @@ def summarize_mfma(counter_csv, trace_csv, out, title, note, cmd):
         g = v["GRBM_GUI_ACTIVE"] / 8.0
         agg[key].append((dur[d], g / dur[d], v["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024.0 / g))
     lines = [f"# {title}", "", note, "", "Command (on the MI355X box, from /tmp with TMPDIR=/tmp; R = repository root):",
-             "", f"    {cmd}", "", "| kernel | dispatches | average µs | clock GHz | MFMA busy |", "|---|---|---|---|---|"]
+             "", f"    {cmd}", "", "| kernel | dispatches | average µs | active cycles per ns | MFMA busy |", "|---|---|---|---|---|"]
     for (k, _), v in sorted(agg.items(), key=lambda kv: -sum(x[0] for x in kv[1])):
         n = len(v)
         avg = sum(x[0] for x in v) / n
